@@ -1,0 +1,181 @@
+/*
+ * wise.h — C ABI of libwise, the gfx950 (MI355X) hot path of WISE
+ * (Working-set Inference with Support Exploitation) for recurrent-depth
+ * language models.
+ *
+ * The method (paper, Section 5): during the first t_d recurrent steps run
+ * full causal attention and pool its probabilities into per
+ * (query-block, key-block) masses (Section 5.1, eq. "block_attention_mass");
+ * pick, per query block, the smallest set of key blocks whose pooled mass
+ * reaches a threshold (Section 5.1, eq. "block_working_set"); for every later
+ * step restrict attention to that fixed block support while Q/K/V are
+ * recomputed (Section 5.2, eq. "wise_attention").  The support is kept as a
+ * device-resident CSR schedule (Appendix B, "Sparse-kernel implementation").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every tensor argument is a DEVICE pointer owned by the caller,
+ *    contiguous, row-major.  The library allocates nothing.
+ *  - bf16 tensors are raw IEEE bfloat16 storage (uint16, round-to-nearest-even
+ *    when produced by the library).
+ *  - Shapes: q, k, v, o are [batch][heads][seq_len][head_dim];
+ *    lse is [batch][heads][seq_len]; acc is [batch][heads][nb][nb] with
+ *    nb = seq_len / block.  CSR row r = (b * heads + h) * nb + qb.
+ *  - Every call validates its arguments on the host BEFORE touching the
+ *    device and returns a status; on any error nothing is launched and no
+ *    output is written.  On success the work is only enqueued on
+ *    `hip_stream` (a hipStream_t, NULL = default stream) and the call
+ *    returns; device-side faults surface at the caller's next
+ *    synchronisation.  WISE_ERR_HIP carries a failed launch.
+ *  - Calls are stateless and re-entrant; calls on different streams with
+ *    disjoint outputs may run concurrently.  No C++ exception crosses the ABI.
+ *  - Supported: head_dim in {64, 96, 128}; block in {64, 128};
+ *    seq_len % block == 0.
+ */
+#ifndef WISE_H
+#define WISE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WISE_ABI_VERSION 1
+
+typedef enum {
+  WISE_OK = 0,
+  WISE_ERR_NULL = 1,        /* a required pointer is NULL                    */
+  WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0,
+                               or a size that overflows int32 indexing       */
+  WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
+  WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, or unknown flag bit */
+  WISE_ERR_WORKSPACE = 5,   /* workspace smaller than wise_select_workspace_bytes */
+  WISE_ERR_HIP = 6          /* a HIP launch reported an error                */
+} wise_status;
+
+/* Problem geometry shared by all calls.  scale <= 0 selects 1/sqrt(head_dim),
+ * the softmax temperature of the paper's attention (Section 3, eq.
+ * "recurrent_attention"). */
+typedef struct {
+  int32_t batch;
+  int32_t heads;
+  int32_t seq_len;
+  int32_t head_dim;
+  int32_t block;
+  float scale;
+} wise_shape;
+
+/* Selection flags: blocks forced into every support after the cumulative-mass
+ * cut.  The paper's own selection is flags = 0; the default used by this
+ * library's callers is WISE_FORCE_SINK | WISE_FORCE_DIAG. */
+enum {
+  WISE_FORCE_SINK = 1u, /* key block 0 (the attention-sink block)     */
+  WISE_FORCE_DIAG = 2u  /* key block qb (the causal diagonal block)   */
+};
+
+/*
+ * wise_dense_attn_accum — full causal attention of one recurrent step,
+ * optionally pooling its probabilities into block masses.
+ *
+ *   O = softmax(Q K^T * scale + M) V,  M the causal mask (key j <= query i)
+ *       (Section 3, eq. "recurrent_attention")
+ *   lse_i = log sum_{j<=i} exp(scale * q_i . k_j)      (natural log)
+ *   if acc != NULL, for every kb <= qb:
+ *     acc[b][h][qb][kb] += (1/block) * sum_{i in I_qb} sum_{j in I_kb, j<=i} A_ij
+ *       (Section 5.1, eq. "block_attention_mass"); entries kb > qb untouched.
+ *
+ *   q, k, v : bf16 [batch][heads][seq_len][head_dim], read-only.
+ *   o       : bf16, same shape, written.
+ *   lse     : fp32 [batch][heads][seq_len] or NULL.  Must be non-NULL when
+ *             acc != NULL (the pooled probabilities use it).
+ *   acc     : fp32 [batch][heads][nb][nb] or NULL (plain dense attention).
+ *             Read-modify-written; the caller zeroes it before the first
+ *             step of the discovery window.  Each acc row is owned by one
+ *             workgroup: no float atomics, bitwise deterministic.
+ * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with lse NULL),
+ *         WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_HIP.
+ */
+wise_status wise_dense_attn_accum(const wise_shape* s, const void* q,
+                                  const void* k, const void* v, void* o,
+                                  float* lse, float* acc, void* hip_stream);
+
+/*
+ * wise_select_support — per query block, the smallest set of key blocks whose
+ * accumulated mass reaches tau of the row total (Section 5.1, eq.
+ * "block_working_set", the arg-min over admissible blocks), plus the blocks
+ * named in `flags`, emitted as CSR.
+ *
+ * Per row (b, h, qb), with v_kb = acc[b][h][qb][kb] for kb = 0..qb:
+ *   1. order the candidates by (v descending, kb ascending);
+ *   2. c_k = sum of the first k ordered masses, summed in that order in
+ *      fp64 (c_0 = 0), total = c_{qb+1};
+ *   3. k* = min{ k >= 0 : c_k >= tau * total }   (fp64);
+ *   4. S = first k* ordered blocks  U  {0 if SINK}  U  {qb if DIAG};
+ *      S empty (total == 0 and flags == 0) -> S = {qb};
+ *   5. col_idx[row_ptr[r] .. row_ptr[r+1]) = S in ascending order.
+ *
+ *   acc       : fp32 [batch][heads][nb][nb], read-only (entries kb > qb ignored).
+ *   tau       : 0 < tau <= 1.
+ *   flags     : OR of WISE_FORCE_* bits.
+ *   row_ptr   : int32 [rows + 1], rows = batch*heads*nb; row_ptr[0] = 0,
+ *               row_ptr[rows] = nnz.
+ *   col_idx   : int32 [wise_support_capacity(s)]; the first nnz are written.
+ *   row_order : int32 [rows] or NULL: the rows sorted by support size
+ *               descending, ties by row id ascending (longest-first schedule
+ *               for wise_sparse_attn; Appendix B, "execution-metadata
+ *               preparation").
+ *   workspace : device scratch of at least wise_select_workspace_bytes(s)
+ *               bytes; contents on entry are ignored.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_RANGE,
+ *         WISE_ERR_WORKSPACE, WISE_ERR_HIP.
+ */
+wise_status wise_select_support(const wise_shape* s, const float* acc,
+                                float tau, uint32_t flags, int32_t* row_ptr,
+                                int32_t* col_idx, int32_t* row_order,
+                                void* workspace, size_t workspace_bytes,
+                                void* hip_stream);
+
+/*
+ * wise_sparse_attn — attention of one late recurrent step restricted to a
+ * block support (Section 5.2, eq. "wise_attention"):
+ *   O = softmax(Q K^T * scale + M + R) V,  R_ij = 0 if kb(j) in S_{qb(i)},
+ *   -inf otherwise.  Q/K/V are this step's; only the support is reused.
+ *
+ *   q, k, v   : bf16 [batch][heads][seq_len][head_dim], read-only.
+ *   row_ptr   : int32 [rows + 1], col_idx : int32 [nnz] — a CSR whose rows
+ *               list key-block ids in strictly ascending order with every id
+ *               <= qb (as written by wise_select_support).  The kernel trusts
+ *               this invariant; it is not re-checked on the device.
+ *   row_order : int32 [rows], a permutation of 0..rows-1 giving the order in
+ *               which rows are scheduled, or NULL for natural order.
+ *   o         : bf16, same shape as q, written.  A row with an empty support
+ *               writes zeros (and lse = -inf).
+ *   lse       : fp32 [batch][heads][seq_len] or NULL.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_HIP.
+ */
+wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k,
+                             const void* v, const int32_t* row_ptr,
+                             const int32_t* col_idx, const int32_t* row_order,
+                             void* o, float* lse, void* hip_stream);
+
+/* Bytes of device workspace wise_select_support needs for shape s
+ * (0 for an invalid shape). */
+size_t wise_select_workspace_bytes(const wise_shape* s);
+
+/* Upper bound on nnz: batch * heads * nb * (nb + 1) / 2, the number of
+ * causally admissible block pairs (-1 for an invalid shape). */
+int64_t wise_support_capacity(const wise_shape* s);
+
+/* Static, NUL-terminated description of a status code. */
+const char* wise_status_string(wise_status st);
+
+/* WISE_ABI_VERSION of the loaded library. */
+int32_t wise_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WISE_H */

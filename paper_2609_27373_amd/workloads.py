@@ -1,0 +1,199 @@
+"""Seeded synthetic workloads for the WISE hot path.
+
+This module only draws inputs; it contains none of the method's arithmetic,
+and both the HIP path and the CPU oracle consume what it produces.
+
+The paper measures on saved working-set workloads of a trained recurrent-depth
+model over a public multi-hop QA benchmark (Section 7.4, Appendix B,
+"Systems evaluation").  Neither the model nor the data is available, so a
+planted generator stands in: per (batch, head) it draws iid keys and values,
+picks for every query block a few "relevant" earlier key blocks, and builds
+each query tile from the mean of those key tiles plus noise, so that the
+attention mass of a query block concentrates on its planted blocks.  Every
+recurrent step then perturbs Q, K and V by a small Gaussian random walk
+(Q^(t) = Q^(t-1) + eps_t), so that Q/K/V keep changing while the routing stays
+roughly put, as in the paper's late steps.
+
+Readings of the workload text (all std, not variance):
+  K0, V0 ~ N(0, 1)[n, d];  Q tile q = g * mean_{r in rel(q)} K0[tile r]
+  + 0.5 * N(0, 1)[B, d];  eps_t ~ 0.02 * N(0, 1).  rel(0) = {0}.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class WorkloadConfig:
+    name: str
+    batch: int
+    heads: int
+    head_dim: int
+    seq_len: int
+    block: int
+    discovery_steps: int      # t_d
+    late_steps: int           # T - t_d
+    taus: Tuple[float, ...]   # selection threshold(s); the first is the default
+    relevant: Tuple[int, int]  # planted blocks per query block, drawn U{lo..hi}
+    sink: bool = False        # also plant key block 0 in every query block
+    zipf: Optional[float] = None  # distance bias p(c) ~ (q - c)^-zipf
+    gain: float = 3.0         # g
+    noise: float = 0.5        # std of the query-tile noise
+    step_noise: float = 0.02  # std of the per-step random walk
+    seed: int = 0
+    dtype: str = "bf16"
+
+    @property
+    def nb(self) -> int:
+        return self.seq_len // self.block
+
+    @property
+    def tau(self) -> float:
+        return self.taus[0]
+
+    @property
+    def steps(self) -> int:
+        return self.discovery_steps + self.late_steps
+
+    @property
+    def window(self) -> Tuple[int, ...]:
+        """1-based discovery steps whose block masses are accumulated: the
+        last min(4, t_d) discovery steps (the paper's window t_d-3..t_d)."""
+        w = min(4, self.discovery_steps)
+        return tuple(range(self.discovery_steps - w + 1, self.discovery_steps + 1))
+
+    def with_(self, **kw) -> "WorkloadConfig":
+        return dataclasses.replace(self, **kw)
+
+
+CONFIGS = {
+    # tiny CPU-checkable case: 2 heads, d 64, n 512, B 64, 4 + 4 steps, tau 0.9
+    "tiny": WorkloadConfig("tiny", 1, 2, 64, 512, 64, 4, 4, (0.9,), (2, 2),
+                           seed=0, dtype="fp32"),
+    # 4K, 32 heads, d 128, B 64, 4 + 28 steps, tau 0.95, 4 planted + sink
+    "4k": WorkloadConfig("4k", 1, 32, 128, 4096, 64, 4, 28, (0.95,), (4, 4),
+                         sink=True, seed=1),
+    # 8K, 55 heads, d 96, B 64, 6 + 26 steps, 6 planted with Zipf(1.2) recency
+    "8k": WorkloadConfig("8k", 1, 55, 96, 8192, 64, 6, 26, (0.95,), (6, 6),
+                         zipf=1.2, seed=2),
+    # 16K, batch 2, 32 heads, d 128, B 128, 4 + 28 steps, tau swept
+    "16k": WorkloadConfig("16k", 2, 32, 128, 16384, 128, 4, 28,
+                          (0.95, 0.8, 0.9, 0.99), (8, 8), seed=3),
+    # 32K, 32 heads, d 128, B 128, 8 + 24 steps, heavy-tailed 1..32 planted
+    "32k": WorkloadConfig("32k", 1, 32, 128, 32768, 128, 8, 24, (0.95,), (1, 32),
+                          seed=4),
+}
+# The 4K case at the sparser routing regime of the paper's systems cohort
+# (density ~0.37-0.45 at 2K-4K, Section 7.5 and Appendix C.6): same generator,
+# gain raised so the planted blocks dominate the attention mass.
+CONFIGS["4k-pr"] = CONFIGS["4k"].with_(name="4k-pr", gain=4.5)
+
+
+def relevant_blocks(cfg: WorkloadConfig) -> list:
+    """Planted key blocks: list over (b*heads + h) of list over qb of int arrays.
+
+    Drawn on the host with numpy from cfg.seed, so the structure is identical
+    whatever device the tensors are later drawn on.
+    """
+    rng = np.random.default_rng(cfg.seed)
+    out = []
+    lo, hi = cfg.relevant
+    for _ in range(cfg.batch * cfg.heads):
+        per_q = []
+        for q in range(cfg.nb):
+            if q == 0:
+                per_q.append(np.array([0]))
+                continue
+            cand = np.arange(q)
+            if cfg.sink:
+                cand = cand[cand != 0]
+            r = int(rng.integers(lo, hi + 1))
+            r = min(r, cand.size)
+            if r > 0:
+                p = None
+                if cfg.zipf is not None:
+                    w = (q - cand).astype(np.float64) ** (-cfg.zipf)
+                    p = w / w.sum()
+                rel = rng.choice(cand, size=r, replace=False, p=p)
+            else:
+                rel = np.zeros(0, dtype=np.int64)
+            if cfg.sink:
+                rel = np.concatenate(([0], rel))
+            per_q.append(np.sort(rel))
+        out.append(per_q)
+    return out
+
+
+def _gen(device, seed: int, tag: int) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1_000_003 + tag) & 0x7FFF_FFFF_FFFF_FFFF)
+    return g
+
+
+def planted_base(cfg: WorkloadConfig, device="cpu", heads: Optional[Sequence[int]] = None):
+    """fp32 (Q0, K0, V0), each [batch][heads][n][d], on `device`.
+
+    `heads` restricts generation to a subset of flattened (b*heads + h) ids
+    (the returned tensors are then [1][len(heads)][n][d]); each head's draws
+    depend only on (seed, head id), so a subset reproduces the full tensor's
+    slices exactly.
+    """
+    n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
+    rel = relevant_blocks(cfg)
+    ids = list(range(cfg.batch * cfg.heads)) if heads is None else list(heads)
+    Q = torch.empty((len(ids), n, d), dtype=torch.float32, device=device)
+    K = torch.empty_like(Q)
+    V = torch.empty_like(Q)
+    for slot, hid in enumerate(ids):
+        g = _gen(device, cfg.seed, 1 + hid)
+        K[slot] = torch.randn((n, d), generator=g, device=device)
+        V[slot] = torch.randn((n, d), generator=g, device=device)
+        W = torch.zeros((nb, nb), dtype=torch.float32)
+        for q, r in enumerate(rel[hid]):
+            W[q, torch.as_tensor(r)] = 1.0 / len(r)
+        W = W.to(device)
+        mean_tiles = W @ K[slot].reshape(nb, B * d)
+        noise = torch.randn((nb, B * d), generator=g, device=device)
+        Q[slot] = (cfg.gain * mean_tiles + cfg.noise * noise).reshape(n, d)
+    if heads is None:
+        shape = (cfg.batch, cfg.heads, n, d)
+    else:
+        shape = (1, len(ids), n, d)
+    return Q.reshape(shape), K.reshape(shape), V.reshape(shape)
+
+
+class Trajectory:
+    """Per-step inputs of one recurrent trajectory.
+
+    Step t (1-based) holds X_t = X_{t-1} + eps_t for X in {Q, K, V}, with
+    X_0 the planted base.  `next()` returns the step's tensors in the
+    working dtype (bf16, round-to-nearest-even, unless cfg.dtype is fp32)
+    and advances; the fp32 random-walk state stays on `device`.  The step
+    noise of each head is drawn from its own (seed, head, step) stream, so a
+    head subset reproduces the full trajectory's slices on the same device.
+    """
+
+    def __init__(self, cfg: WorkloadConfig, device="cpu", heads=None):
+        self.cfg = cfg
+        self.device = device
+        self.ids = list(range(cfg.batch * cfg.heads)) if heads is None else list(heads)
+        self.state = list(planted_base(cfg, device, heads))
+        self.t = 0
+
+    def next(self, dtype=None):
+        self.t += 1
+        n, d = self.cfg.seq_len, self.cfg.head_dim
+        for slot, hid in enumerate(self.ids):
+            g = _gen(self.device, self.cfg.seed, (1 + hid) * 65536 + self.t)
+            for x in self.state:
+                flat = x.view(-1, n, d)
+                flat[slot].add_(torch.randn((n, d), generator=g, device=self.device),
+                                alpha=self.cfg.step_noise)
+        dt = dtype or (torch.float32 if self.cfg.dtype == "fp32" else torch.bfloat16)
+        return tuple(x.to(dt).contiguous() for x in self.state)
