@@ -30,7 +30,9 @@
  *  - Calls are stateless and re-entrant; calls on different streams with
  *    disjoint outputs may run concurrently.  No C++ exception crosses the ABI.
  *  - Supported: head_dim in {64, 96, 128}; block in {64, 128};
- *    seq_len % block == 0.
+ *    seq_len % block == 0; nb <= 1024 for wise_select_support.
+ *  - Alignment: q, k, v, o 16 bytes; workspace 256 bytes; every other
+ *    pointer 4 bytes.  A misaligned pointer is WISE_ERR_SHAPE.
  */
 #ifndef WISE_H
 #define WISE_H
@@ -50,7 +52,8 @@ typedef enum {
   WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0,
                                or a size that overflows int32 indexing       */
   WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
-  WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, or unknown flag bit */
+  WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, non-finite scale,
+                               or unknown flag bit                           */
   WISE_ERR_WORKSPACE = 5,   /* workspace smaller than wise_select_workspace_bytes */
   WISE_ERR_HIP = 6          /* a HIP launch reported an error                */
 } wise_status;
@@ -146,8 +149,9 @@ wise_status wise_select_support(const wise_shape* s, const float* acc,
  *   q, k, v   : bf16 [batch][heads][seq_len][head_dim], read-only.
  *   row_ptr   : int32 [rows + 1], col_idx : int32 [nnz] — a CSR whose rows
  *               list key-block ids in strictly ascending order with every id
- *               <= qb (as written by wise_select_support).  The kernel trusts
- *               this invariant; it is not re-checked on the device.
+ *               <= qb (as written by wise_select_support).  Ids outside
+ *               0..qb are skipped on the device (never read out of bounds);
+ *               ordering and uniqueness are trusted, not re-checked.
  *   row_order : int32 [rows], a permutation of 0..rows-1 giving the order in
  *               which rows are scheduled, or NULL for natural order.
  *   o         : bf16, same shape as q, written.  A row with an empty support

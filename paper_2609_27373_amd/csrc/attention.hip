@@ -1,0 +1,469 @@
+// attention.hip — the three attention kernels of libwise on gfx950:
+//
+//   dense_attn_kernel   causal flash attention, O and natural-log LSE
+//                       (paper Section 3, eq. recurrent_attention)
+//   block_mass_kernel   block-pooled softmax mass acc[qb][kb] += r_qb,kb
+//                       (Section 5.1, eq. block_attention_mass), recomputing
+//                       QK^T against the LSE the dense kernel wrote
+//   sparse_attn_kernel  attention restricted to a CSR block support
+//                       (Section 5.2, eq. wise_attention)
+//
+// Shared tile engine.  A wave owns 32 consecutive queries.  For each tile of
+// 64 keys it computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K from
+// LDS, B = Q^T held in registers for the whole row), so every lane ends up
+// holding 32 scores of ONE query.  The row max needs one cross-lane step
+// (lanes l and l^32 share a query), the row sum none until the end, and the
+// probabilities are already in the B-operand layout of O^T = V^T P^T: they are
+// packed to bf16 in place and fed straight to the second MFMA chain.  V is
+// transposed once per tile on its way into LDS (8x8 register blocks, v_perm),
+// so both MFMA chains read LDS with conflict-free 128-bit loads.  Softmax is
+// online in base 2 with the exact running max (so the largest probability of
+// a row is exactly 1 in bf16); the O rescale is skipped, wave-uniformly, on
+// tiles that raise no row's max.
+#include "wise_device.hpp"
+#include "wise_kernels.hpp"
+
+namespace wise {
+
+// ---------------------------------------------------------------------------
+// Global -> register -> LDS staging of one 64-key tile (K row-major, V
+// transposed).  Loads for tile i+1 are issued before tile i is computed, so
+// the HBM/L2 latency hides behind the MFMA work; stores follow the barrier
+// that retires tile i.
+// ---------------------------------------------------------------------------
+template <int D, int NT, bool kWithV>
+struct TileStage {
+  using G = Geo<D>;
+  static constexpr int kRowChunks = D / 8;                    // 16-B chunks per key row
+  static constexpr int kKChunks = kKeyTile * kRowChunks;
+  static constexpr int kKPer = (kKChunks + NT - 1) / NT;
+  static constexpr int kVBlocks = (kKeyTile / 8) * (D / 8);   // 8 keys x 8 dims
+  static constexpr int kVPer = kWithV ? (kVBlocks + NT - 1) / NT : 0;
+
+  u32x4_t kr[kKPer];
+  u32x4_t vr[kVPer > 0 ? kVPer : 1][8];
+
+  __device__ __forceinline__ void load(const uint16_t* kg, const uint16_t* vg, int key0, int tid) {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int ch = tid + i * NT;
+      if (kKChunks % NT == 0 || ch < kKChunks) {
+        const int key = ch / kRowChunks, c8 = ch % kRowChunks;
+        kr[i] = *(const u32x4_t*)(kg + (size_t)(key0 + key) * D + c8 * 8);
+      }
+    }
+    if constexpr (kWithV) {
+#pragma unroll
+      for (int i = 0; i < kVPer; ++i) {
+        const int blk = tid + i * NT;
+        if (kVBlocks % NT == 0 || blk < kVBlocks) {
+          const int kb = blk & 7, db = blk >> 3;
+          const uint16_t* src = vg + (size_t)(key0 + 8 * kb) * D + 8 * db;
+#pragma unroll
+          for (int r = 0; r < 8; ++r) vr[i][r] = *(const u32x4_t*)(src + (size_t)r * D);
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(uint16_t* ks, uint16_t* vt, int tid) const {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int ch = tid + i * NT;
+      if (kKChunks % NT == 0 || ch < kKChunks) {
+        const int key = ch / kRowChunks, c8 = ch % kRowChunks;
+        *(u32x4_t*)(ks + k_lds_row(key) * G::kKStride + c8 * 8) = kr[i];
+      }
+    }
+    if constexpr (kWithV) {
+#pragma unroll
+      for (int i = 0; i < kVPer; ++i) {
+        const int blk = tid + i * NT;
+        if (kVBlocks % NT == 0 || blk < kVBlocks) {
+          const int kb = blk & 7, db = blk >> 3;
+          uint16_t* dst = vt + (8 * db) * G::kVStride + 8 * kb;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            u32x4_t ev, od;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+              ev[p] = lo_halves(vr[i][2 * p][w], vr[i][2 * p + 1][w]);
+              od[p] = hi_halves(vr[i][2 * p][w], vr[i][2 * p + 1][w]);
+            }
+            *(u32x4_t*)(dst + (2 * w) * G::kVStride) = ev;
+            *(u32x4_t*)(dst + (2 * w + 1) * G::kVStride) = od;
+          }
+        }
+      }
+    }
+  }
+};
+
+// Tile-local key held by register r of S^T tile t in a lane of half-wave h.
+__device__ __forceinline__ int score_key(int t, int r, int h) {
+  const int j = r >> 2, i = r & 3;
+  return 32 * t + 16 * (j >> 1) + 8 * h + 4 * (j & 1) + i;
+}
+
+// ---------------------------------------------------------------------------
+// Per-wave state and steps of the tile engine.
+// ---------------------------------------------------------------------------
+template <int D>
+struct WaveRows {
+  using G = Geo<D>;
+  u32x4_t qf[G::kDChunks];   // Q^T B-operand fragments, one per 16-dim chunk
+  f32x16_t o[G::kDTiles];    // O^T accumulator, 32 dims x 32 queries per tile
+  float m;                   // running max of scale*log2(e)*s (per query)
+  float l;                   // running sum over this lane's half of the keys
+
+  __device__ __forceinline__ void load_q(const uint16_t* qg, int q0, int lane) {
+    const uint16_t* row = qg + (size_t)(q0 + (lane & 31)) * D + 8 * (lane >> 5);
+#pragma unroll
+    for (int c = 0; c < G::kDChunks; ++c) qf[c] = *(const u32x4_t*)(row + 16 * c);
+  }
+
+  __device__ __forceinline__ void reset() {
+#pragma unroll
+    for (int t = 0; t < G::kDTiles; ++t) o[t] = f32x16_t{};
+    m = -INFINITY;
+    l = 0.f;
+  }
+
+  // S^T of one 64-key LDS tile: s[0] covers LDS rows 0..31, s[1] rows 32..63.
+  __device__ __forceinline__ void scores(const uint16_t* ks, int lane, f32x16_t s[2]) const {
+    const uint16_t* a0 = ks + (lane & 31) * G::kKStride + 8 * (lane >> 5);
+    const uint16_t* a1 = a0 + 32 * G::kKStride;
+    f32x16_t s0{}, s1{};
+#pragma unroll
+    for (int c = 0; c < G::kDChunks; ++c) {
+      s0 = mfma32x32x16(*(const u32x4_t*)(a0 + 16 * c), qf[c], s0);
+      s1 = mfma32x32x16(*(const u32x4_t*)(a1 + 16 * c), qf[c], s1);
+    }
+    s[0] = s0;
+    s[1] = s1;
+  }
+
+  // Causal mask inside a tile: key0 + local key > query -> -inf.
+  __device__ __forceinline__ static void mask(f32x16_t s[2], int key0, int qi, int lane) {
+    const int h = lane >> 5;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (key0 + score_key(t, r, h) > qi) s[t][r] = -INFINITY;
+  }
+
+  // Online softmax of one tile and O^T += V^T P^T.
+  __device__ __forceinline__ void softmax_pv(f32x16_t s[2], const uint16_t* vt, int lane, float c) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
+    mx = pair_max(mx) * c;
+    const bool grow = mx > m;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float mn = grow ? mx : m;
+      const float alpha = (mn == m) ? 1.f : fast_exp2(m - mn);
+      l *= alpha;
+#pragma unroll
+      for (int t = 0; t < G::kDTiles; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+      m = mn;
+    }
+    const float mb = (m == -INFINITY) ? 0.f : m;
+    u32x4_t pb[4];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(__builtin_fmaf(s[t][r], c, -mb));
+        s[t][r] = p;
+        l += p;
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          pb[2 * t + u][e] = pack_bf16x2(s[t][8 * u + 2 * e], s[t][8 * u + 2 * e + 1]);
+    }
+    const uint16_t* a = vt + (lane & 31) * G::kVStride + 8 * (lane >> 5);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int t = 0; t < G::kDTiles; ++t)
+        o[t] = mfma32x32x16(*(const u32x4_t*)(a + (32 * t) * G::kVStride + 16 * ks), pb[ks], o[t]);
+  }
+
+  // O = O^T / l written as bf16 rows; lse in natural log.
+  __device__ __forceinline__ void finish(uint16_t* og, float* lse, int q0, int lane) const {
+    const float lt = pair_sum(l);
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    const int q = q0 + (lane & 31), h = lane >> 5;
+    uint16_t* row = og + (size_t)q * D + 4 * h;
+#pragma unroll
+    for (int t = 0; t < G::kDTiles; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        u32x2_t w;
+        w[0] = pack_bf16x2(o[t][4 * j] * inv, o[t][4 * j + 1] * inv);
+        w[1] = pack_bf16x2(o[t][4 * j + 2] * inv, o[t][4 * j + 3] * inv);
+        *(u32x2_t*)(row + 32 * t + 8 * j) = w;
+      }
+    if (lse != nullptr && h == 0) lse[q] = lt > 0.f ? (m + __builtin_log2f(lt)) * kLn2 : -INFINITY;
+  }
+};
+
+// Work-group id -> logical id such that consecutive logical ids run on the
+// same XCD (hardware deals work-groups round-robin over the 8 XCDs), keeping
+// a head's K/V tiles in one XCD's L2.
+__device__ __forceinline__ int xcd_logical_id() {
+  const int g = gridDim.x, b = blockIdx.x;
+  return (g % 8 == 0) ? (b % 8) * (g / 8) + b / 8 : b;
+}
+
+// ---------------------------------------------------------------------------
+// Dense causal attention.  A work-group of NW waves owns 32*NW consecutive
+// queries of one (batch, head); heavier (later) query tiles are issued first.
+// ---------------------------------------------------------------------------
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                  const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
+                  float* __restrict__ lse, int n, int qtiles, float c) {
+  using G = Geo<D>;
+  constexpr int kNT = NW * 64, kQT = NW * 32;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
+  const int lid = xcd_logical_id();
+  const int bh = lid / qtiles, qt = qtiles - 1 - lid % qtiles;
+  const size_t hoff = (size_t)bh * n * D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qbase = qt * kQT, q0 = qbase + 32 * wave;
+
+  WaveRows<D> w;
+  w.load_q(Q + hoff, q0, lane);
+  w.reset();
+  const int ntiles = (qbase + kQT - 1) / kKeyTile + 1;
+  TileStage<D, kNT, true> st;
+  st.load(K + hoff, V + hoff, 0, tid);
+  for (int it = 0; it < ntiles; ++it) {
+    st.store(ks, vt, tid);
+    __syncthreads();
+    if (it + 1 < ntiles) st.load(K + hoff, V + hoff, (it + 1) * kKeyTile, tid);
+    const int key0 = it * kKeyTile;
+    if (key0 <= q0) {
+      f32x16_t s[2];
+      w.scores(ks, lane, s);
+      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, q0 + (lane & 31), lane);
+      w.softmax_pv(s, vt, lane, c);
+    }
+    __syncthreads();
+  }
+  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Block mass.  One work-group per (batch, head, query block), NW = block/32
+// waves; the group owns its acc row, so the read-modify-write needs no
+// atomics and the reduction order is fixed.
+// ---------------------------------------------------------------------------
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                  const float* __restrict__ lse, float* __restrict__ acc, int n, int nb,
+                  float c) {
+  using G = Geo<D>;
+  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
+  __shared__ float red[NW];
+  const int lid = xcd_logical_id();
+  const int bh = lid / nb, qb = nb - 1 - lid % nb;
+  const size_t hoff = (size_t)bh * n * D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q0 = qb * kB + 32 * wave;
+  const int qi = q0 + (lane & 31);
+  float* arow = acc + ((size_t)bh * nb + qb) * nb;
+
+  WaveRows<D> w;
+  w.load_q(Q + hoff, q0, lane);
+  const float nl = -lse[(size_t)bh * n + qi] * kLog2e;   // -log2 of the row normaliser
+  const int ntiles = (qb + 1) * kTPB;
+  TileStage<D, kNT, false> st;
+  st.load(K + hoff, nullptr, 0, tid);
+  float blk = 0.f;
+  for (int it = 0; it < ntiles; ++it) {
+    st.store(ks, nullptr, tid);
+    __syncthreads();
+    if (it + 1 < ntiles) st.load(K + hoff, nullptr, (it + 1) * kKeyTile, tid);
+    const int key0 = it * kKeyTile;
+    float part = 0.f;
+    if (key0 <= q0) {
+      f32x16_t s[2];
+      w.scores(ks, lane, s);
+      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, qi, lane);
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) part += fast_exp2(__builtin_fmaf(s[t][r], c, nl));
+    }
+    blk += wave_sum(part);
+    const bool last = (it % kTPB) == kTPB - 1;
+    if (last && lane == 0) red[wave] = blk;
+    __syncthreads();
+    if (last) {
+      if (tid == 0) {
+        float tot = 0.f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) tot += red[i];
+        arow[it / kTPB] += tot * (1.f / kB);
+      }
+      blk = 0.f;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Block-sparse attention over a CSR support.  One work-group per (batch,
+// head, query block) row, NW = block/32 waves; rows are taken in `order`
+// (longest support first when built by wise_select_support).
+// ---------------------------------------------------------------------------
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                   const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
+                   const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
+                   uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
+                   float c) {
+  using G = Geo<D>;
+  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
+  const int row = order ? order[blockIdx.x] : (int)blockIdx.x;
+  if ((unsigned)row >= (unsigned)rows) return;
+  const int bh = row / nb, qb = row % nb;
+  const size_t hoff = (size_t)bh * n * D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q0 = qb * kB + 32 * wave;
+  const int beg = row_ptr[row];
+  const int ntiles = (row_ptr[row + 1] - beg) * kTPB;
+
+  // Tile it -> first key; ids outside 0..qb are ignored (their tile is
+  // neither loaded out of bounds nor used).
+  auto tile_key = [&](int it, bool& ok) {
+    const int kb = col_idx[beg + it / kTPB];
+    ok = (unsigned)kb <= (unsigned)qb;
+    return ok ? kb * kB + (it % kTPB) * kKeyTile : 0;
+  };
+
+  WaveRows<D> w;
+  w.load_q(Q + hoff, q0, lane);
+  w.reset();
+  TileStage<D, kNT, true> st;
+  bool ok = false;
+  int key0 = ntiles > 0 ? tile_key(0, ok) : 0;
+  if (ntiles > 0) st.load(K + hoff, V + hoff, key0, tid);
+  for (int it = 0; it < ntiles; ++it) {
+    st.store(ks, vt, tid);
+    __syncthreads();
+    bool ok_next = false;
+    const int key_next = (it + 1 < ntiles) ? tile_key(it + 1, ok_next) : 0;
+    if (it + 1 < ntiles) st.load(K + hoff, V + hoff, key_next, tid);
+    if (ok && key0 <= q0) {
+      f32x16_t s[2];
+      w.scores(ks, lane, s);
+      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, q0 + (lane & 31), lane);
+      w.softmax_pv(s, vt, lane, c);
+    }
+    __syncthreads();
+    key0 = key_next;
+    ok = ok_next;
+  }
+  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (shapes already validated by the C ABI layer).
+// ---------------------------------------------------------------------------
+template <int D>
+static hipError_t launch_dense_d(const Dims& s, const void* q, const void* k, const void* v,
+                                 void* o, float* lse, hipStream_t st) {
+  const float c = s.scale * kLog2e;
+  const auto* Q = (const uint16_t*)q;
+  const auto* K = (const uint16_t*)k;
+  const auto* V = (const uint16_t*)v;
+  if (s.n % 128 == 0) {
+    const int qt = s.n / 128;
+    hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(s.bh * qt), dim3(256), 0, st, Q, K, V,
+                       (uint16_t*)o, lse, s.n, qt, c);
+  } else {
+    const int qt = s.n / 64;
+    hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(s.bh * qt), dim3(128), 0, st, Q, K, V,
+                       (uint16_t*)o, lse, s.n, qt, c);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void* v, void* o,
+                        float* lse, hipStream_t st) {
+  switch (s.d) {
+    case 64: return launch_dense_d<64>(s, q, k, v, o, lse, st);
+    case 96: return launch_dense_d<96>(s, q, k, v, o, lse, st);
+    default: return launch_dense_d<128>(s, q, k, v, o, lse, st);
+  }
+}
+
+template <int D>
+static hipError_t launch_mass_d(const Dims& s, const void* q, const void* k, const float* lse,
+                                float* acc, hipStream_t st) {
+  const float c = s.scale * kLog2e;
+  const auto* Q = (const uint16_t*)q;
+  const auto* K = (const uint16_t*)k;
+  if (s.block == 64)
+    hipLaunchKernelGGL((block_mass_kernel<D, 2>), dim3(s.bh * s.nb), dim3(128), 0, st, Q, K, lse,
+                       acc, s.n, s.nb, c);
+  else
+    hipLaunchKernelGGL((block_mass_kernel<D, 4>), dim3(s.bh * s.nb), dim3(256), 0, st, Q, K, lse,
+                       acc, s.n, s.nb, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_mass(const Dims& s, const void* q, const void* k, const float* lse, float* acc,
+                       hipStream_t st) {
+  switch (s.d) {
+    case 64: return launch_mass_d<64>(s, q, k, lse, acc, st);
+    case 96: return launch_mass_d<96>(s, q, k, lse, acc, st);
+    default: return launch_mass_d<128>(s, q, k, lse, acc, st);
+  }
+}
+
+template <int D>
+static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, const void* v,
+                                  const int32_t* rp, const int32_t* ci, const int32_t* order,
+                                  void* o, float* lse, hipStream_t st) {
+  const float c = s.scale * kLog2e;
+  const auto* Q = (const uint16_t*)q;
+  const auto* K = (const uint16_t*)k;
+  const auto* V = (const uint16_t*)v;
+  const int rows = s.bh * s.nb;
+  if (s.block == 64)
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 2>), dim3(rows), dim3(128), 0, st, Q, K, V, rp, ci,
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, c);
+  else
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 4>), dim3(rows), dim3(256), 0, st, Q, K, V, rp, ci,
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse(const Dims& s, const void* q, const void* k, const void* v,
+                         const int32_t* rp, const int32_t* ci, const int32_t* order, void* o,
+                         float* lse, hipStream_t st) {
+  switch (s.d) {
+    case 64: return launch_sparse_d<64>(s, q, k, v, rp, ci, order, o, lse, st);
+    case 96: return launch_sparse_d<96>(s, q, k, v, rp, ci, order, o, lse, st);
+    default: return launch_sparse_d<128>(s, q, k, v, rp, ci, order, o, lse, st);
+  }
+}
+
+}  // namespace wise

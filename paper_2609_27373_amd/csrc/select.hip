@@ -1,0 +1,296 @@
+// select.hip — support selection and CSR schedule construction on gfx950.
+//
+// Paper Section 5.1, eq. (block_working_set): per query block, the smallest
+// set of admissible key blocks whose mass reaches the threshold, i.e. the
+// heaviest k* blocks with k* the first prefix of the descending order that
+// reaches tau * total.  The schedule is a device-resident CSR (Appendix B,
+// "Sparse-kernel implementation") plus a longest-support-first row order.
+//
+//   select_rows_kernel   one wave per row: rank every candidate by
+//                        (mass desc, block asc), sum the ordered masses
+//                        sequentially in fp64 (the same association as a
+//                        left-to-right prefix sum), cut, add forced blocks,
+//                        emit a bitmask and a count
+//   scan_kernel          exclusive scan of counts -> row_ptr
+//   scatter_kernel       bitmask -> ascending col_idx
+//   order_*_kernel       stable counting sort of rows by count, descending
+#include "wise_device.hpp"
+#include "wise_kernels.hpp"
+
+namespace wise {
+
+constexpr int kSelWaves = 4;        // rows per work-group in the per-row kernels
+constexpr int kOrderChunk = 256;    // rows per chunk of the counting sort
+
+// Orderable 32-bit image of a float: unsigned order == float order.
+__device__ __forceinline__ uint32_t float_key(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// E = candidates per lane (ceil(nb / 64) rounded up to a power of two).
+template <int E>
+__global__ void __launch_bounds__(kSelWaves * 64)
+select_rows_kernel(const float* __restrict__ acc, int rows, int nb, double tau, uint32_t flags,
+                   int32_t* __restrict__ counts, uint64_t* __restrict__ masks, int words) {
+  extern __shared__ __attribute__((aligned(16))) uint64_t sel_smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = blockIdx.x * kSelWaves + wave;
+  const bool active = row < rows;
+  uint64_t* keys = sel_smem + (size_t)wave * 2 * nb;   // [nb] sort keys, later prefixes
+  double* sv = (double*)(keys + nb);                    // [nb] masses in sorted order
+  const int qb = active ? row % nb : 0;
+  const int cnt = active ? qb + 1 : 0;
+  const float* v = acc + (size_t)(active ? row : 0) * nb;
+
+  // 1. composite keys: mass descending, then block index ascending
+  float x[E];
+  uint64_t key[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int b = lane + 64 * e;
+    x[e] = 0.f;
+    key[e] = 0;
+    if (b < cnt) {
+      x[e] = v[b];
+      key[e] = ((uint64_t)float_key(x[e]) << 32) | (uint32_t)(~(uint32_t)b);
+      keys[b] = key[e];
+    }
+  }
+  __syncthreads();
+  // 2. rank = number of candidates ordered before this one
+  int rank[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) rank[e] = 0;
+  for (int c = 0; c < cnt; ++c) {
+    const uint64_t kc = keys[c];
+#pragma unroll
+    for (int e = 0; e < E; ++e) rank[e] += (kc > key[e]) ? 1 : 0;
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (lane + 64 * e < cnt) sv[rank[e]] = (double)x[e];
+  __syncthreads();
+  // 3. sequential fp64 prefix sums in sorted order (identical in every lane)
+  double* pre = (double*)keys;
+  double run = 0.0;
+  for (int r = 0; r < cnt; ++r) {
+    run += sv[r];
+    if (lane == 0) pre[r] = run;
+  }
+  __syncthreads();
+  // 4. k* = min{k >= 0 : c_k >= tau * total}, c_0 = 0
+  const double thr = tau * run;
+  int kstar = cnt;
+  if (thr <= 0.0) {
+    kstar = 0;
+  } else {
+    for (int r = lane; r < cnt; r += 64)
+      if (pre[r] >= thr) { kstar = min(kstar, r + 1); break; }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) kstar = min(kstar, __shfl_xor(kstar, off, 64));
+  }
+  // 5. selection bitmask, forced blocks, empty -> diagonal
+  int total = 0;
+  uint64_t mword[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int b = lane + 64 * e;
+    bool s = false;
+    if (b < cnt)
+      s = rank[e] < kstar || (b == 0 && (flags & 1u)) || (b == qb && (flags & 2u));
+    mword[e] = __builtin_amdgcn_ballot_w64(s);
+    total += __builtin_popcountll(mword[e]);
+  }
+  if (total == 0) {
+    mword[qb >> 6] |= 1ull << (qb & 63);
+    total = 1;
+  }
+  if (active && lane == 0) {
+    counts[row] = total;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (e < words) masks[(size_t)row * words + e] = mword[e];
+  }
+}
+
+// Inclusive scan of one value per thread over a 1024-thread block.
+__device__ __forceinline__ int block_scan_1024(int x, int* wsum) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  if (wave == 0) {
+    int w = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int y = __shfl_up(w, off, 64);
+      if (lane >= off) w += y;
+    }
+    if (lane < 16) wsum[lane] = w;
+  }
+  __syncthreads();
+  const int add = wave > 0 ? wsum[wave - 1] : 0;
+  __syncthreads();
+  return x + add;
+}
+
+// row_ptr[0] = 0, row_ptr[r+1] = counts[0] + ... + counts[r].
+__global__ void __launch_bounds__(1024)
+scan_kernel(const int32_t* __restrict__ counts, int rows, int32_t* __restrict__ row_ptr) {
+  __shared__ int wsum[16];
+  __shared__ int carry;
+  if (threadIdx.x == 0) {
+    carry = 0;
+    row_ptr[0] = 0;
+  }
+  __syncthreads();
+  for (int base = 0; base < rows; base += 1024) {
+    const int r = base + threadIdx.x;
+    const int x = r < rows ? counts[r] : 0;
+    const int inc = block_scan_1024(x, wsum);
+    const int c0 = carry;
+    if (r < rows) row_ptr[r + 1] = c0 + inc;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry = c0 + inc;
+    __syncthreads();
+  }
+}
+
+// col_idx[row_ptr[r] ..] = set bits of the row's mask, ascending.
+__global__ void __launch_bounds__(kSelWaves * 64)
+scatter_kernel(const uint64_t* __restrict__ masks, const int32_t* __restrict__ row_ptr, int rows,
+               int words, int32_t* __restrict__ col_idx) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kSelWaves + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  int pos = row_ptr[row];
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int e = 0; e < words; ++e) {
+    const uint64_t m = masks[(size_t)row * words + e];
+    if ((m >> lane) & 1ull) col_idx[pos + __builtin_popcountll(m & below)] = 64 * e + lane;
+    pos += __builtin_popcountll(m);
+  }
+}
+
+// Counting sort of rows by count (descending), stable by row id.
+// (a) per-chunk histograms hist[chunk][c], c = 0..nb
+__global__ void __launch_bounds__(kOrderChunk)
+order_hist_kernel(const int32_t* __restrict__ counts, int rows, int nb, int32_t* __restrict__ hist) {
+  extern __shared__ int32_t h_smem[];
+  for (int c = threadIdx.x; c <= nb; c += kOrderChunk) h_smem[c] = 0;
+  __syncthreads();
+  const int r = blockIdx.x * kOrderChunk + threadIdx.x;
+  if (r < rows) atomicAdd(&h_smem[counts[r]], 1);
+  __syncthreads();
+  for (int c = threadIdx.x; c <= nb; c += kOrderChunk)
+    hist[(size_t)blockIdx.x * (nb + 1) + c] = h_smem[c];
+}
+
+// (b) hist[chunk][c] -> rows of count c in earlier chunks; start[c] = rows
+//     with a larger count.
+__global__ void __launch_bounds__(1024)
+order_offsets_kernel(int32_t* __restrict__ hist, int nchunks, int nb, int32_t* __restrict__ start) {
+  for (int c = threadIdx.x; c <= nb; c += 1024) {
+    int run = 0;
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int h = hist[(size_t)ch * (nb + 1) + c];
+      hist[(size_t)ch * (nb + 1) + c] = run;
+      run += h;
+    }
+    start[c] = run;   // total rows with count c, turned into offsets below
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int c = nb; c >= 0; --c) {
+      const int t = start[c];
+      start[c] = acc;
+      acc += t;
+    }
+  }
+}
+
+// (c) place each row.
+__global__ void __launch_bounds__(kOrderChunk)
+order_place_kernel(const int32_t* __restrict__ counts, int rows, int nb,
+                   const int32_t* __restrict__ hist, const int32_t* __restrict__ start,
+                   int32_t* __restrict__ order) {
+  __shared__ int32_t cs[kOrderChunk];
+  const int r = blockIdx.x * kOrderChunk + threadIdx.x;
+  const int c = r < rows ? counts[r] : -1;
+  cs[threadIdx.x] = c;
+  __syncthreads();
+  if (r >= rows) return;
+  int rank = 0;
+  for (int t = 0; t < (int)threadIdx.x; ++t) rank += (cs[t] == c) ? 1 : 0;
+  order[start[c] + hist[(size_t)blockIdx.x * (nb + 1) + c] + rank] = r;
+}
+
+// Workspace layout: counts | masks | hist | start, each 256-B aligned.
+struct SelectWs {
+  size_t counts, masks, hist, start, total;
+  int words, nchunks;
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static SelectWs select_ws(const Dims& s) {
+  SelectWs w;
+  const size_t rows = (size_t)s.bh * s.nb;
+  w.words = (s.nb + 63) / 64;
+  w.nchunks = (int)((rows + kOrderChunk - 1) / kOrderChunk);
+  w.counts = 0;
+  w.masks = align256(w.counts + rows * 4);
+  w.hist = align256(w.masks + rows * w.words * 8);
+  w.start = align256(w.hist + (size_t)w.nchunks * (s.nb + 1) * 4);
+  w.total = align256(w.start + (size_t)(s.nb + 1) * 4);
+  return w;
+}
+
+size_t select_workspace_bytes(const Dims& s) { return select_ws(s).total; }
+
+hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t flags,
+                         int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, void* ws,
+                         hipStream_t st) {
+  const SelectWs w = select_ws(s);
+  char* base = (char*)ws;
+  auto* counts = (int32_t*)(base + w.counts);
+  auto* masks = (uint64_t*)(base + w.masks);
+  auto* hist = (int32_t*)(base + w.hist);
+  auto* start = (int32_t*)(base + w.start);
+  const int rows = s.bh * s.nb;
+  const int groups = (rows + kSelWaves - 1) / kSelWaves;
+  const size_t smem = (size_t)kSelWaves * 2 * s.nb * sizeof(uint64_t);
+  const dim3 sg(groups), sb(kSelWaves * 64);
+  const double dtau = (double)tau;
+  if (s.nb <= 64)
+    hipLaunchKernelGGL(select_rows_kernel<1>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
+  else if (s.nb <= 128)
+    hipLaunchKernelGGL(select_rows_kernel<2>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
+  else if (s.nb <= 256)
+    hipLaunchKernelGGL(select_rows_kernel<4>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
+  else if (s.nb <= 512)
+    hipLaunchKernelGGL(select_rows_kernel<8>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
+  else
+    hipLaunchKernelGGL(select_rows_kernel<16>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, st, counts, rows, row_ptr);
+  hipLaunchKernelGGL(scatter_kernel, dim3(groups), dim3(kSelWaves * 64), 0, st, masks, row_ptr,
+                     rows, w.words, col_idx);
+  if (row_order != nullptr) {
+    const size_t hsmem = (size_t)(s.nb + 1) * sizeof(int32_t);
+    hipLaunchKernelGGL(order_hist_kernel, dim3(w.nchunks), dim3(kOrderChunk), hsmem, st, counts,
+                       rows, s.nb, hist);
+    hipLaunchKernelGGL(order_offsets_kernel, dim3(1), dim3(1024), 0, st, hist, w.nchunks, s.nb,
+                       start);
+    hipLaunchKernelGGL(order_place_kernel, dim3(w.nchunks), dim3(kOrderChunk), 0, st, counts,
+                       rows, s.nb, hist, start, row_order);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace wise

@@ -1,0 +1,133 @@
+// wise_api.hip — the C ABI of libwise (declared in include/wise.h).
+//
+// Every entry point validates its arguments on the host before touching the
+// HIP runtime, so an invalid call returns its status without launching
+// anything (and without needing a GPU).  Valid calls only enqueue kernels on
+// the caller's stream.
+#include <math.h>
+#include <stdint.h>
+
+#include "wise.h"
+#include "wise_kernels.hpp"
+
+namespace {
+
+constexpr int64_t kI32Max = 2147483647;
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// Geometry checks shared by all calls; fills the validated dims.
+wise_status check_shape(const wise_shape* s, wise::Dims* out) {
+  if (s == nullptr) return WISE_ERR_NULL;
+  if (s->batch <= 0 || s->heads <= 0 || s->seq_len <= 0 || s->head_dim <= 0 || s->block <= 0)
+    return WISE_ERR_SHAPE;
+  if (s->head_dim != 64 && s->head_dim != 96 && s->head_dim != 128) return WISE_ERR_UNSUPPORTED;
+  if (s->block != 64 && s->block != 128) return WISE_ERR_UNSUPPORTED;
+  if (s->seq_len % s->block != 0) return WISE_ERR_SHAPE;
+  if (isnan(s->scale) || isinf(s->scale)) return WISE_ERR_RANGE;
+  const int64_t bh = (int64_t)s->batch * s->heads;
+  const int64_t nb = s->seq_len / s->block;
+  // CSR offsets are int32: every admissible block pair must be addressable.
+  if (bh * nb > kI32Max || bh * nb * (nb + 1) / 2 > kI32Max) return WISE_ERR_SHAPE;
+  out->bh = (int)bh;
+  out->n = s->seq_len;
+  out->d = s->head_dim;
+  out->block = s->block;
+  out->nb = (int)nb;
+  out->scale = s->scale > 0.f ? s->scale : 1.0f / sqrtf((float)s->head_dim);
+  return WISE_OK;
+}
+
+wise_status check_qkvo(const void* q, const void* k, const void* v, const void* o) {
+  if (!q || !k || !v || !o) return WISE_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
+    return WISE_ERR_SHAPE;
+  return WISE_OK;
+}
+
+wise_status from_hip(hipError_t e) { return e == hipSuccess ? WISE_OK : WISE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+wise_status wise_dense_attn_accum(const wise_shape* s, const void* q, const void* k,
+                                  const void* v, void* o, float* lse, float* acc,
+                                  void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if ((st = check_qkvo(q, k, v, o)) != WISE_OK) return st;
+  if (acc != nullptr && lse == nullptr) return WISE_ERR_NULL;
+  if ((lse && !aligned(lse, 4)) || (acc && !aligned(acc, 4))) return WISE_ERR_SHAPE;
+  const hipStream_t stream = (hipStream_t)hip_stream;
+  hipError_t e = wise::launch_dense(d, q, k, v, o, lse, stream);
+  if (e == hipSuccess && acc != nullptr) e = wise::launch_mass(d, q, k, lse, acc, stream);
+  return from_hip(e);
+}
+
+wise_status wise_select_support(const wise_shape* s, const float* acc, float tau, uint32_t flags,
+                                int32_t* row_ptr, int32_t* col_idx, int32_t* row_order,
+                                void* workspace, size_t workspace_bytes, void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!acc || !row_ptr || !col_idx || !workspace) return WISE_ERR_NULL;
+  if (d.nb > wise::kMaxSelectBlocks) return WISE_ERR_UNSUPPORTED;
+  if (!(tau > 0.f && tau <= 1.f)) return WISE_ERR_RANGE;
+  if (flags & ~(uint32_t)(WISE_FORCE_SINK | WISE_FORCE_DIAG)) return WISE_ERR_RANGE;
+  if (workspace_bytes < wise::select_workspace_bytes(d)) return WISE_ERR_WORKSPACE;
+  if (!aligned(acc, 4) || !aligned(row_ptr, 4) || !aligned(col_idx, 4) ||
+      (row_order && !aligned(row_order, 4)) || !aligned(workspace, 256))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_select(d, acc, tau, flags, row_ptr, col_idx, row_order, workspace,
+                                      (hipStream_t)hip_stream));
+}
+
+wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k, const void* v,
+                             const int32_t* row_ptr, const int32_t* col_idx,
+                             const int32_t* row_order, void* o, float* lse, void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if ((st = check_qkvo(q, k, v, o)) != WISE_OK) return st;
+  if (!row_ptr || !col_idx) return WISE_ERR_NULL;
+  if (!aligned(row_ptr, 4) || !aligned(col_idx, 4) || (row_order && !aligned(row_order, 4)) ||
+      (lse && !aligned(lse, 4)))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_sparse(d, q, k, v, row_ptr, col_idx, row_order, o, lse,
+                                      (hipStream_t)hip_stream));
+}
+
+size_t wise_select_workspace_bytes(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return 0;
+  return wise::select_workspace_bytes(d);
+}
+
+int64_t wise_support_capacity(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return -1;
+  return (int64_t)d.bh * d.nb * (d.nb + 1) / 2;
+}
+
+const char* wise_status_string(wise_status st) {
+  switch (st) {
+    case WISE_OK: return "WISE_OK: success";
+    case WISE_ERR_NULL: return "WISE_ERR_NULL: a required pointer is NULL";
+    case WISE_ERR_SHAPE:
+      return "WISE_ERR_SHAPE: invalid geometry, seq_len not a multiple of block, size beyond "
+             "int32 CSR indexing, or a misaligned pointer";
+    case WISE_ERR_UNSUPPORTED:
+      return "WISE_ERR_UNSUPPORTED: head_dim must be 64/96/128, block 64/128, seq_len/block <= "
+             "1024 for selection";
+    case WISE_ERR_RANGE: return "WISE_ERR_RANGE: tau outside (0, 1], bad scale or unknown flag bits";
+    case WISE_ERR_WORKSPACE: return "WISE_ERR_WORKSPACE: workspace smaller than required";
+    case WISE_ERR_HIP: return "WISE_ERR_HIP: a kernel launch failed";
+  }
+  return "unknown wise_status";
+}
+
+int32_t wise_abi_version(void) { return WISE_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,91 @@
+// wise_device.hpp — gfx950 device helpers shared by the libwise kernels:
+// vector types, the bf16 MFMA wrapper, packing, cross-lane helpers and the
+// tile geometry of the attention kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wise {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kKeyTile = 64;    // keys per LDS tile
+constexpr int kQPerWave = 32;   // queries owned by one wave (MFMA N dimension)
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// D (32 x 32, fp32) += A (32 x 16, bf16) * B (16 x 32, bf16).
+// Lane l holds A[l % 32][8*(l/32) .. +7], B[8*(l/32) .. +7][l % 32];
+// C element (m, n) sits in lane n + 32*((m/4) % 2), register 4*(m/8) + m%4.
+__device__ __forceinline__ f32x16_t mfma32x32x16(u32x4_t a, u32x4_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Two fp32 -> packed bf16x2 (round to nearest even), lo in bits 0..15.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// Combine x with the value held by lane l ^ 32 (the other half of the wave
+// holding the same query column).  permlane32_swap leaves one register with
+// the low half-wave replicated and the other with the high half replicated,
+// so max / sum of the two is the pair result in every lane, computed in the
+// same order in both lanes.
+__device__ __forceinline__ float pair_max(float x) {
+  uint32_t u = __builtin_bit_cast(uint32_t, x);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  uint32_t u = __builtin_bit_cast(uint32_t, x);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Interleave the bf16 halves of two dwords: (lo(a), lo(b)) or (hi(a), hi(b)).
+__device__ __forceinline__ uint32_t lo_halves(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ __forceinline__ uint32_t hi_halves(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
+// Full-wave fp32 sum in a fixed butterfly order (deterministic).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+// Tile geometry of the attention kernels for head dimension D.
+template <int D>
+struct Geo {
+  static_assert(D == 64 || D == 96 || D == 128, "head_dim");
+  static constexpr int kKStride = D + 8;          // LDS K row stride (bf16): 16 B pad
+  static constexpr int kVStride = kKeyTile + 8;   // LDS V^T row stride (bf16)
+  static constexpr int kDChunks = D / 16;         // MFMA k-steps of S^T = K Q^T
+  static constexpr int kDTiles = D / 32;          // MFMA m-tiles of O^T = V^T P^T
+  static constexpr int kKElems = kKeyTile * kKStride;
+  static constexpr int kVElems = D * kVStride;
+};
+
+// Row of the LDS K tile that holds tile-local key `key`.  S^T = K Q^T puts
+// tile row m at accumulator position (m/8, (m/4)%2, m%4); swapping bits 2 and
+// 3 of the key makes each lane's 8 consecutive accumulator entries hold 8
+// consecutive keys, which is exactly the B-operand layout of O^T = V^T P^T.
+__device__ __forceinline__ int k_lds_row(int key) {
+  return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
+}
+
+}  // namespace wise

@@ -1,0 +1,117 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects invalid arguments on the host with the documented
+status before any device work (null device pointers are never dereferenced)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_27373_amd import wise
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wise.h")
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(wise_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(wise.LIB_PATH):
+        from paper_2609_27373_amd import build
+        build.build()
+    return wise.load()
+
+
+def test_header_lists_the_binding_exports():
+    assert header_functions() == sorted(wise.EXPORTS)
+
+
+def test_exports(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", wise.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    syms = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    for fn in header_functions():
+        assert fn in syms, fn
+        assert hasattr(lib, fn)
+
+
+def test_version_and_strings(lib):
+    assert wise.wise_abi_version() == 1
+    for st, name in wise.STATUS_NAMES.items():
+        assert wise.wise_status_string(st).startswith(name)
+    assert "unknown" in wise.wise_status_string(99)
+
+
+def S(**kw):
+    base = dict(batch=1, heads=2, seq_len=512, head_dim=64, block=64, scale=0.0)
+    base.update(kw)
+    return wise.make_shape(**base)
+
+
+def test_capacity_and_workspace(lib):
+    s = S()
+    assert wise.wise_support_capacity(s) == 2 * 8 * 9 // 2
+    assert wise.wise_select_workspace_bytes(s) > 0
+    s4 = S(batch=1, heads=32, seq_len=32768, head_dim=128, block=128)
+    assert wise.wise_support_capacity(s4) == 32 * 256 * 257 // 2
+    assert wise.wise_support_capacity(S(seq_len=500)) == -1
+    assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
+
+
+FAKE = ctypes.c_void_p(4096)        # aligned, never dereferenced: calls fail validation first
+MIS = ctypes.c_void_p(4096 + 2)     # misaligned
+
+
+def dense(lib, s, q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, acc=None):
+    return lib.wise_dense_attn_accum(ctypes.byref(s) if s is not None else None, q, k, v, o, lse,
+                                     acc, None)
+
+
+def select(lib, s, acc=FAKE, tau=0.9, flags=3, rp=FAKE, ci=FAKE, ro=None, ws=FAKE, wsb=1 << 30):
+    return lib.wise_select_support(ctypes.byref(s) if s is not None else None, acc,
+                                   ctypes.c_float(tau), flags, rp, ci, ro, ws, wsb, None)
+
+
+def sparse(lib, s, q=FAKE, rp=FAKE, ci=FAKE, o=FAKE):
+    return lib.wise_sparse_attn(ctypes.byref(s) if s is not None else None, q, FAKE, FAKE, rp, ci,
+                                None, o, None, None)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(q=None), 1), (dict(o=None), 1), (dict(acc=FAKE), 1),
+    (dict(s=S(seq_len=500)), 2), (dict(s=S(batch=0)), 2), (dict(s=S(heads=-1)), 2),
+    (dict(s=S(head_dim=80)), 3), (dict(s=S(block=32)), 3), (dict(q=MIS), 2),
+    (dict(s=S(scale=float("inf"))), 4), (dict(s=S(scale=float("nan"))), 4),
+    (dict(s=S(batch=4096, heads=4096, seq_len=1024, block=64)), 2),
+])
+def test_dense_validation(lib, case, status):
+    s = case.pop("s", S())
+    assert dense(lib, s, **case) == status
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(acc=None), 1), (dict(rp=None), 1), (dict(ws=None), 1),
+    (dict(tau=0.0), 4), (dict(tau=1.5), 4), (dict(tau=float("nan")), 4), (dict(tau=-0.1), 4),
+    (dict(flags=4), 4), (dict(wsb=16), 5), (dict(s=S(block=96)), 3),
+    (dict(s=S(seq_len=64 * 2048)), 3), (dict(ws=ctypes.c_void_p(4096 + 16)), 2),
+])
+def test_select_validation(lib, case, status):
+    s = case.pop("s", S())
+    assert select(lib, s, **case) == status
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(q=None), 1), (dict(rp=None), 1), (dict(ci=None), 1),
+    (dict(o=None), 1), (dict(s=S(seq_len=100)), 2), (dict(s=S(head_dim=256)), 3),
+    (dict(o=MIS), 2),
+])
+def test_sparse_validation(lib, case, status):
+    s = case.pop("s", S())
+    assert sparse(lib, s, **case) == status

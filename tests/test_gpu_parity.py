@@ -1,0 +1,325 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded, bf16-rounded inputs.
+
+Bars (from the task's targets):
+  attention outputs  max-abs <= 1e-2 and mean-abs <= 1e-3 vs the oracle.
+                     The outputs are bf16: rounding them alone costs up to
+                     half a bf16 spacing, 2^-7 for |O| in [2, 4) but 2^-6 in
+                     [4, 8), which exceeds 1e-2 by itself.  So the max-abs bar
+                     applies where |ref| < 4, and where |ref| >= 4 (a row
+                     concentrated on one value row beyond 4 sigma) the error
+                     must stay within one bf16 spacing, 2^-7 |ref|.
+  LSE                max-abs <= 1e-3 (natural log)
+  accumulator        max-abs <= 1e-5 per window step (masses lie in [0, 1])
+  CSR / row order    bit-exact; an end-to-end CSR row may differ only when
+                     the oracle's own cut is within 1e-5 of a boundary (the
+                     margins delta^-, delta^+, delta^rank of Appendix A),
+                     and such rows are reported, not failed.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import wise_oracle as O
+from paper_2609_27373_amd.workloads import CONFIGS, Trajectory
+
+pytestmark = pytest.mark.gpu
+
+ATOL_MAX, ATOL_MEAN, LSE_TOL, ACC_TOL, TIE = 1e-2, 1e-3, 1e-3, 1e-5, 1e-5
+
+
+def f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def attn_errors(gpu, ref):
+    g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
+    err = np.abs(g - ref)
+    big = np.abs(ref) >= 4.0
+    small_max = err[~big].max() if (~big).any() else 0.0
+    big_ratio = (err[big] / (2.0 ** -7 * np.abs(ref[big]))).max() if big.any() else 0.0
+    return err, small_max, big_ratio, int(big.sum())
+
+
+def assert_attn(gpu, ref, what=""):
+    err, small_max, big_ratio, nbig = attn_errors(gpu, ref)
+    say(f"  {what}: max-abs {err.max():.3g} (|ref|<4: {small_max:.3g}; {nbig} outputs |ref|>=4 "
+        f"at {big_ratio:.2f} spacing) mean-abs {err.mean():.3g}")
+    assert small_max <= ATOL_MAX and big_ratio <= 1.0 and err.mean() <= ATOL_MEAN, \
+        f"{what}: max {err.max():.3g} (small {small_max:.3g}, big {big_ratio:.2f}) mean {err.mean():.3g}"
+
+
+def assert_lse(gpu, ref, what=""):
+    g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
+    both_inf = np.isneginf(g) & np.isneginf(ref)
+    err = np.abs(np.where(both_inf, 0.0, g - ref))
+    assert err.max() <= LSE_TOL, f"{what}: lse max {err.max():.3g}"
+
+
+def rows_of(rp, ci):
+    rp = rp.cpu().numpy() if isinstance(rp, torch.Tensor) else rp
+    ci = ci.cpu().numpy() if isinstance(ci, torch.Tensor) else ci
+    return [list(ci[rp[r]:rp[r + 1]]) for r in range(len(rp) - 1)]
+
+
+def near_tie(v, qb, tau):
+    m = O.support_margins(v, qb, tau)
+    return min(m["delta_minus"], m["delta_plus"], m["delta_rank"]) < TIE
+
+
+def compare_support(gpu_rows, acc_ref, tau, flags, row_ids=None):
+    """End-to-end CSR rows vs the oracle's selection on its own accumulator."""
+    bt, h, nb, _ = acc_ref.shape
+    flat = acc_ref.reshape(bt * h * nb, nb)
+    reported = []
+    ids = range(bt * h * nb) if row_ids is None else row_ids
+    for i, r in enumerate(ids):
+        qb = r % nb
+        want = O.select_row(flat[r], qb, tau, flags)
+        got = [int(x) for x in gpu_rows[i]]
+        if got != want:
+            assert near_tie(flat[r], qb, tau), f"row {r}: gpu {got} oracle {want}"
+            reported.append(r)
+    if reported:
+        say(f"near-tie CSR rows reported (not failed): {reported[:20]} ({len(reported)})")
+    return reported
+
+
+def random_support(nb_rows, nb, rng, bh, with_diag=0.7):
+    rp, ci = [0], []
+    for _ in range(bh):
+        for qb in range(nb):
+            k = int(rng.integers(1, qb + 2))
+            s = set(rng.choice(qb + 1, size=k, replace=False).tolist())
+            if rng.random() < with_diag:
+                s.add(qb)
+            ci.extend(sorted(s))
+            rp.append(len(ci))
+    return np.array(rp, np.int32), np.array(ci, np.int32)
+
+
+def inputs(bt, h, n, d, seed, scale=1.0, planted=False):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn((bt, h, n, d), generator=g) * scale
+    k = torch.randn((bt, h, n, d), generator=g)
+    v = torch.randn((bt, h, n, d), generator=g)
+    if planted:   # make some rows peaky so the lazy rescale path triggers
+        q[..., ::7, :] *= 4
+    return [x.to(torch.bfloat16) for x in (q, k, v)]
+
+
+SHAPES = [  # bt, h, n, d, B  (ragged: n not a multiple of 128, single block, ...)
+    (1, 1, 64, 64, 64), (2, 3, 384, 64, 64), (1, 2, 320, 96, 64), (1, 2, 640, 128, 64),
+    (2, 2, 512, 128, 128), (1, 3, 384, 96, 128), (1, 1, 128, 64, 128), (1, 2, 1024, 128, 64),
+]
+
+
+@pytest.mark.parametrize("bt,h,n,d,B", SHAPES)
+def test_dense_and_mass(gpu_lib, bt, h, n, d, B):
+    w = gpu_lib
+    say(f"dense+mass bt={bt} h={h} n={n} d={d} B={B}")
+    q, k, v = inputs(bt, h, n, d, seed=n + d + B, scale=1.5)
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    nb = n // B
+    acc = torch.full((bt, h, nb, nb), 0.25, device="cuda")   # RMW onto a non-zero start
+    w.wise_dense_attn_accum(s, q.cuda(), k.cuda(), v.cuda(), o, lse, acc)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.dense_attention(f64(q), f64(k), f64(v))
+    assert_attn(o, o_ref, "dense O")
+    assert_lse(lse, l_ref, "dense lse")
+    r_ref = O.block_mass(f64(q), f64(k), B)
+    a = f64(acc) - 0.25
+    upper = np.triu(np.ones((nb, nb), bool), 1)
+    assert np.all(a[..., upper] == 0), "entries past the diagonal must stay untouched"
+    assert np.abs(a - r_ref).max() <= ACC_TOL, np.abs(a - r_ref).max()
+
+
+@pytest.mark.parametrize("bt,h,n,d,B", SHAPES)
+def test_sparse_random_support(gpu_lib, bt, h, n, d, B):
+    w = gpu_lib
+    say(f"sparse bt={bt} h={h} n={n} d={d} B={B}")
+    q, k, v = inputs(bt, h, n, d, seed=7 * n + d, scale=1.5)
+    nb = n // B
+    rng = np.random.default_rng(n * d)
+    rp, ci = random_support(None, nb, rng, bt * h)
+    order = O.schedule_order(rp)
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    for ord_t in (None, torch.from_numpy(order).cuda()):
+        w.wise_sparse_attn(s, q.cuda(), k.cuda(), v.cuda(), torch.from_numpy(rp).cuda(),
+                           torch.from_numpy(ci).cuda(), ord_t, o, lse)
+        torch.cuda.synchronize()
+        o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp, ci, B)
+        assert_attn(o, o_ref, "sparse O")
+        assert_lse(lse, l_ref, "sparse lse")
+
+
+@pytest.mark.parametrize("d,B", [(64, 64), (128, 64), (96, 128)])
+def test_peaky_rows(gpu_lib, d, B):
+    """Near one-hot rows (queries scaled x6): the running max jumps by large
+    amounts between tiles, so the O rescale path runs often, and O is close to
+    single value rows, some beyond 4 in magnitude."""
+    w = gpu_lib
+    bt, h, n = 1, 2, 512
+    q, k, v = inputs(bt, h, n, d, seed=99 + d, scale=1.0)
+    q = (q.float() * 6).to(torch.bfloat16)
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    w.wise_dense_attn_accum(s, q.cuda(), k.cuda(), v.cuda(), o, lse, None)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.dense_attention(f64(q), f64(k), f64(v))
+    assert_attn(o, o_ref, "peaky O")
+    assert_lse(lse, l_ref, "peaky lse")
+
+
+@pytest.mark.parametrize("d,B", [(64, 64), (96, 64), (128, 64), (128, 128), (96, 128)])
+def test_full_support_sparse_equals_dense(gpu_lib, d, B):
+    """With every causal block in the support, R = 0 and the sparse kernel
+    computes the dense result; the per-query tile order and arithmetic are the
+    same, so the outputs agree bit for bit."""
+    w = gpu_lib
+    bt, h, n = 1, 2, 768
+    q, k, v = (x.cuda() for x in inputs(bt, h, n, d, seed=d + B, scale=1.5, planted=True))
+    nb = n // B
+    rp, ci = [0], []
+    for _ in range(bt * h):
+        for qb in range(nb):
+            ci.extend(range(qb + 1))
+            rp.append(len(ci))
+    s = w.make_shape(bt, h, n, d, B)
+    od, os_ = torch.empty_like(q), torch.empty_like(q)
+    ld, ls = torch.empty((bt, h, n), device="cuda"), torch.empty((bt, h, n), device="cuda")
+    w.wise_dense_attn_accum(s, q, k, v, od, ld, None)
+    w.wise_sparse_attn(s, q, k, v, torch.tensor(rp, dtype=torch.int32, device="cuda"),
+                       torch.tensor(ci, dtype=torch.int32, device="cuda"), None, os_, ls)
+    torch.cuda.synchronize()
+    assert torch.equal(od, os_)
+    assert torch.equal(ld, ls)
+
+
+def test_sparse_edge_rows(gpu_lib):
+    """Empty rows give O = 0 and lse = -inf; ids past the diagonal are skipped."""
+    w = gpu_lib
+    bt, h, n, d, B = 1, 1, 256, 64, 64
+    q, k, v = inputs(bt, h, n, d, seed=3)
+    rp = np.array([0, 1, 1, 3, 6], np.int32)         # row 1 empty
+    ci = np.array([0, 1, 2, 0, 2, 3], np.int32)      # rows: [0], [], [1, 2], [0, 2, 3]
+    ci_bad = ci.copy()
+    ci_bad[2] = 3                                     # row 2 now names block 3 > qb = 2
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn(s, q.cuda(), k.cuda(), v.cuda(), torch.from_numpy(rp).cuda(),
+                       torch.from_numpy(ci_bad).cuda(), None, o, lse)
+    torch.cuda.synchronize()
+    ci_eff = np.array([0, 1, 0, 2, 3], np.int32)
+    rp_eff = np.array([0, 1, 1, 2, 5], np.int32)
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp_eff, ci_eff, B)
+    assert torch.all(o[0, 0, 64:128] == 0)
+    assert torch.all(torch.isneginf(lse[0, 0, 64:128]))
+    assert_attn(o, o_ref, "edge sparse O")
+    assert_lse(lse, l_ref, "edge lse")
+
+
+@pytest.mark.parametrize("nb,seed", [(1, 0), (8, 1), (63, 2), (64, 3), (65, 4), (128, 5),
+                                     (200, 6), (256, 7), (513, 8), (1024, 9)])
+def test_select_only_parity(gpu_lib, nb, seed):
+    """Selection on identical fp32 masses: CSR and row order are bit-exact."""
+    w = gpu_lib
+    rng = np.random.default_rng(seed)
+    h = 3 if nb <= 256 else 1
+    acc = rng.gamma(0.25, size=(1, h, nb, nb)).astype(np.float32)
+    acc[rng.random(acc.shape) < 0.15] = 0.0
+    acc[..., 1::3] = np.round(acc[..., 1::3], 1)        # exact ties between blocks
+    if nb >= 8:
+        acc[0, 0, 5, :] = 0.0                           # an all-zero row
+    s = w.make_shape(1, h, nb * 64, 64, 64)
+    sched = w.Schedule(s)
+    for tau in (0.5, 0.9, 0.95, 1.0):
+        for flags in (0, 1, 3):
+            t32 = float(np.float32(tau))
+            sched.select(torch.from_numpy(acc).cuda(), t32, flags)
+            torch.cuda.synchronize()
+            rp_ref, ci_ref = O.select_support(acc.astype(np.float64), t32, flags)
+            nnz = sched.nnz()
+            assert np.array_equal(sched.row_ptr.cpu().numpy(), rp_ref), (tau, flags)
+            assert np.array_equal(sched.col_idx[:nnz].cpu().numpy(), ci_ref), (tau, flags)
+            assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp_ref))
+
+
+def test_tiny_trajectory(gpu_lib):
+    """The whole path on the tiny workload: 4 discovery steps (all in the
+    window), selection, 4 late steps; everything against the oracle."""
+    from paper_2609_27373_amd.pipeline import WisePipeline
+    cfg = CONFIGS["tiny"]
+    tr = Trajectory(cfg)
+    pipe = WisePipeline.for_config(cfg)
+    masses = []
+    for t in range(1, cfg.steps + 1):
+        q, k, v = (x.to(torch.bfloat16) for x in tr.next())
+        qg, kg, vg = q.cuda(), k.cuda(), v.cuda()
+        out = torch.empty_like(qg)
+        qd, kd, vd = f64(q), f64(k), f64(v)
+        if t <= cfg.discovery_steps:
+            pipe.discovery_step(qg, kg, vg, out, accumulate=t in cfg.window)
+            torch.cuda.synchronize()
+            o_ref, l_ref = O.dense_attention(qd, kd, vd)
+            assert_attn(out, o_ref, f"step {t} dense")
+            assert_lse(pipe.lse, l_ref, f"step {t} lse")
+            if t in cfg.window:
+                masses.append(O.block_mass(qd, kd, cfg.block))
+                acc_ref = O.accumulate(masses)
+                assert np.abs(f64(pipe.acc) - acc_ref).max() <= ACC_TOL * len(masses)
+            if t == cfg.discovery_steps:
+                sched = pipe.select()
+                torch.cuda.synchronize()
+                tau = float(np.float32(cfg.tau))
+                compare_support(rows_of(sched.row_ptr, sched.col_idx[: sched.nnz()]), acc_ref,
+                                tau, pipe.flags)
+                # selection-only: the GPU's own accumulator through the oracle
+                rp_o, ci_o = O.select_support(f64(pipe.acc), tau, pipe.flags)
+                assert np.array_equal(sched.row_ptr.cpu().numpy(), rp_o)
+                rp, ci = sched.row_ptr.cpu().numpy(), sched.col_idx[: sched.nnz()].cpu().numpy()
+        else:
+            lse = torch.empty_like(pipe.lse)
+            pipe.late_step(qg, kg, vg, out, lse)
+            torch.cuda.synchronize()
+            o_ref, l_ref = O.sparse_attention(qd, kd, vd, rp, ci, cfg.block)
+            assert_attn(out, o_ref, f"step {t} sparse")
+            assert_lse(lse, l_ref, f"step {t} sparse lse")
+            om, _ = O.sparse_attention_masked(qd, kd, vd, rp, ci, cfg.block)
+            assert_attn(out, om, f"step {t} sparse vs masked-dense form")
+
+
+def test_determinism(gpu_lib):
+    from paper_2609_27373_amd.pipeline import WisePipeline
+    cfg = CONFIGS["tiny"].with_(heads=4, seq_len=1024)
+    outs = []
+    for _ in range(2):
+        tr = Trajectory(cfg, device="cuda")
+        pipe = WisePipeline.for_config(cfg)
+        o = None
+        for t in range(1, 6):
+            q, k, v = tr.next(torch.bfloat16)
+            o = torch.empty_like(q)
+            if t <= 4:
+                pipe.discovery_step(q, k, v, o, accumulate=True)
+                if t == 4:
+                    pipe.select()
+            else:
+                pipe.late_step(q, k, v, o)
+        torch.cuda.synchronize()
+        s = pipe.schedule
+        outs.append((o.clone(), pipe.acc.clone(), s.row_ptr.clone(),
+                     s.col_idx[: s.nnz()].clone(), s.row_order.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)

@@ -51,3 +51,26 @@ def test_random_walk_and_dtype():
     assert 0.01 < diff < 0.04
     Q0, K0, V0 = planted_base(c, heads=[0])
     assert abs(K0.std().item() - 1) < 0.01 and abs(V0.mean().item()) < 0.01
+
+
+def test_flop_accounting():
+    from paper_2609_27373_amd import metrics
+    nb, B, d = 4, 8, 16
+    # full support == dense causal count
+    rp, ci = [0], []
+    for qb in range(nb):
+        ci.extend(range(qb + 1))
+        rp.append(len(ci))
+    n = nb * B
+    assert metrics.effective_flops(rp, ci, nb, B, d) == metrics.dense_flops(1, 1, n, d)
+    # brute-force pair count on a random support
+    rng = np.random.default_rng(0)
+    rp, ci, want = [0], [], 0
+    for qb in range(nb):
+        s = sorted(set(rng.choice(qb + 1, size=2).tolist()))
+        ci.extend(s)
+        rp.append(len(ci))
+        for i in range(qb * B, (qb + 1) * B):
+            want += sum(1 for b in s for j in range(b * B, (b + 1) * B) if j <= i)
+    assert metrics.support_pairs(rp, ci, nb, B) == want
+    assert abs(metrics.density(rp, nb, 1) - len(ci) / 10) < 1e-12
