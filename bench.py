@@ -197,6 +197,9 @@ def main():
     ap.add_argument("--config", default="4k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-regime", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="before timing, run one plain device copy of this many MiB (a "
+                         "known-size reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the WISE hot path here runs on a single "
@@ -205,6 +208,14 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     wise.load()
+    if args.copy_calib_mib:
+        src = torch.empty(args.copy_calib_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {args.copy_calib_mib} MiB read + written")
+        del src, dst
     cfg = CONFIGS[args.config]
     log(f"[bench] {cfg.name}: generating {cfg.steps} steps of inputs")
     main_res = measure(cfg, args.steps, args.warmup)
