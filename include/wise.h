@@ -125,10 +125,10 @@ wise_status wise_dense_attn_accum(const wise_shape* s, const void* q,
  *   row_ptr   : int32 [rows + 1], rows = batch*heads*nb; row_ptr[0] = 0,
  *               row_ptr[rows] = nnz.
  *   col_idx   : int32 [wise_support_capacity(s)]; the first nnz are written.
- *   row_order : int32 [rows] or NULL: the rows sorted by support size
- *               descending, ties by row id ascending (longest-first schedule
- *               for wise_sparse_attn; Appendix B, "execution-metadata
- *               preparation").
+ *   row_order : int32 [rows] or NULL: the schedule for wise_sparse_attn
+ *               (Appendix B, "execution-metadata preparation"): rows grouped
+ *               by (batch, head) in ascending order, and within a head by
+ *               support size descending, ties by row id ascending.
  *   workspace : device scratch of at least wise_select_workspace_bytes(s)
  *               bytes; contents on entry are ignored.
  * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_RANGE,
@@ -152,8 +152,11 @@ wise_status wise_select_support(const wise_shape* s, const float* acc,
  *               <= qb (as written by wise_select_support).  Ids outside
  *               0..qb are skipped on the device (never read out of bounds);
  *               ordering and uniqueness are trusted, not re-checked.
- *   row_order : int32 [rows], a permutation of 0..rows-1 giving the order in
- *               which rows are scheduled, or NULL for natural order.
+ *   row_order : int32 [rows], a permutation of 0..rows-1, or NULL for the
+ *               identity.  Schedule slot s runs row row_order[s]; slots are
+ *               dealt to the 8 XCDs in contiguous ranges (slot s on XCD
+ *               s / (rows / 8) when rows % 8 == 0), so rows of one head placed
+ *               together share an L2.
  *   o         : bf16, same shape as q, written.  A row with an empty support
  *               writes zeros (and lse = -inf).
  *   lse       : fp32 [batch][heads][seq_len] or NULL.

@@ -16,7 +16,7 @@ fusion or reordering beyond what the definition states:
                           set, plus forced sink / diagonal blocks
   select_support_union    Section 5.1, eq. (block_working_set), the paper's
                           temporal union of per-step supports
-  schedule_order          longest-support-first ordering of CSR rows
+  schedule_order          per-head longest-support-first ordering of CSR rows
   sparse_attention        Section 5.2, eq. (wise_attention), gather form
   sparse_attention_masked Section 5.2, eq. (wise_attention) with the mask R
   support_margins         the nondegeneracy margins delta^-, delta^+,
@@ -200,12 +200,13 @@ def select_support_union(step_masses, tau, flags=FORCE_SINK | FORCE_DIAG):
     return np.asarray(row_ptr, dtype=np.int32), np.asarray(col_idx, dtype=np.int32)
 
 
-def schedule_order(row_ptr):
-    """Rows sorted by support size descending, ties by row id ascending."""
+def schedule_order(row_ptr, nb):
+    """Rows grouped by (batch, head) = row // nb ascending; within a head by
+    support size descending, ties by row id ascending."""
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     nnz = np.diff(row_ptr)
     rid = np.arange(nnz.size)
-    return np.lexsort((rid, -nnz)).astype(np.int32)
+    return np.lexsort((rid, -nnz, rid // nb)).astype(np.int32)
 
 
 def support_margins(v, qb, tau):

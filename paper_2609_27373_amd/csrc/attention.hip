@@ -14,9 +14,10 @@
 // holding 32 scores of ONE query.  The row max needs one cross-lane step
 // (lanes l and l^32 share a query), the row sum none until the end, and the
 // probabilities are already in the B-operand layout of O^T = V^T P^T: they are
-// packed to bf16 in place and fed straight to the second MFMA chain.  V is
-// transposed once per tile on its way into LDS (8x8 register blocks, v_perm),
-// so both MFMA chains read LDS with conflict-free 128-bit loads.  Softmax is
+// packed to bf16 in place and fed straight to the second MFMA chain.  V stays
+// row-major in LDS and its A-operand fragments are read transposed with
+// ds_read_b64_tr_b16; the 32-byte row pad makes those reads, like the 128-bit
+// K reads, free of bank conflicts.  Softmax is
 // online in base 2 with the exact running max (so the largest probability of
 // a row is exactly 1 in bf16); the O rescale is skipped, wave-uniformly, on
 // tiles that raise no row's max.
@@ -26,74 +27,49 @@
 namespace wise {
 
 // ---------------------------------------------------------------------------
-// Global -> register -> LDS staging of one 64-key tile (K row-major, V
-// transposed).  Loads for tile i+1 are issued before tile i is computed, so
-// the HBM/L2 latency hides behind the MFMA work; stores follow the barrier
-// that retires tile i.
+// Global -> register -> LDS staging of one 64-key tile (K rows permuted so the
+// S^T accumulator comes out in PV operand order; V rows in natural order).
+// Loads for the next tile are issued before the current one is computed, so
+// the memory latency hides behind the MFMA work; stores follow the barrier
+// that retires the current tile.
 // ---------------------------------------------------------------------------
 template <int D, int NT, bool kWithV>
 struct TileStage {
   using G = Geo<D>;
   static constexpr int kRowChunks = D / 8;                    // 16-B chunks per key row
-  static constexpr int kKChunks = kKeyTile * kRowChunks;
-  static constexpr int kKPer = (kKChunks + NT - 1) / NT;
-  static constexpr int kVBlocks = (kKeyTile / 8) * (D / 8);   // 8 keys x 8 dims
-  static constexpr int kVPer = kWithV ? (kVBlocks + NT - 1) / NT : 0;
+  static constexpr int kChunks = kKeyTile * kRowChunks;       // per tensor
+  static constexpr int kPer = (kChunks + NT - 1) / NT;
 
-  u32x4_t kr[kKPer];
-  u32x4_t vr[kVPer > 0 ? kVPer : 1][8];
+  u32x4_t kr[kPer];
+  u32x4_t vr[kWithV ? kPer : 1];
 
-  __device__ __forceinline__ void load(const uint16_t* kg, const uint16_t* vg, int key0, int tid) {
+  // Chunk i of this thread: key row ch / kRowChunks, column (ch % kRowChunks) * 8.
+  __device__ __forceinline__ static int chunk(int tid, int i) { return tid + i * NT; }
+  __device__ __forceinline__ static bool live(int tid, int i) {
+    return kChunks % NT == 0 || chunk(tid, i) < kChunks;
+  }
+
+  // kt, vt: this tile's first key row (uniform); per-lane offsets are 32-bit.
+  __device__ __forceinline__ void load(const uint16_t* kt, const uint16_t* vt, int tid) {
 #pragma unroll
-    for (int i = 0; i < kKPer; ++i) {
-      const int ch = tid + i * NT;
-      if (kKChunks % NT == 0 || ch < kKChunks) {
-        const int key = ch / kRowChunks, c8 = ch % kRowChunks;
-        kr[i] = *(const u32x4_t*)(kg + (size_t)(key0 + key) * D + c8 * 8);
-      }
-    }
-    if constexpr (kWithV) {
-#pragma unroll
-      for (int i = 0; i < kVPer; ++i) {
-        const int blk = tid + i * NT;
-        if (kVBlocks % NT == 0 || blk < kVBlocks) {
-          const int kb = blk & 7, db = blk >> 3;
-          const uint16_t* src = vg + (size_t)(key0 + 8 * kb) * D + 8 * db;
-#pragma unroll
-          for (int r = 0; r < 8; ++r) vr[i][r] = *(const u32x4_t*)(src + (size_t)r * D);
-        }
+    for (int i = 0; i < kPer; ++i) {
+      if (live(tid, i)) {
+        const int ch = chunk(tid, i);
+        const uint32_t off = (uint32_t)((ch / kRowChunks) * D + (ch % kRowChunks) * 8);
+        kr[i] = *(const u32x4_t*)(kt + off);
+        if constexpr (kWithV) vr[i] = *(const u32x4_t*)(vt + off);
       }
     }
   }
 
-  __device__ __forceinline__ void store(uint16_t* ks, uint16_t* vt, int tid) const {
+  __device__ __forceinline__ void store(uint16_t* ks, uint16_t* vs, int tid) const {
 #pragma unroll
-    for (int i = 0; i < kKPer; ++i) {
-      const int ch = tid + i * NT;
-      if (kKChunks % NT == 0 || ch < kKChunks) {
-        const int key = ch / kRowChunks, c8 = ch % kRowChunks;
-        *(u32x4_t*)(ks + k_lds_row(key) * G::kKStride + c8 * 8) = kr[i];
-      }
-    }
-    if constexpr (kWithV) {
-#pragma unroll
-      for (int i = 0; i < kVPer; ++i) {
-        const int blk = tid + i * NT;
-        if (kVBlocks % NT == 0 || blk < kVBlocks) {
-          const int kb = blk & 7, db = blk >> 3;
-          uint16_t* dst = vt + (8 * db) * G::kVStride + 8 * kb;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            u32x4_t ev, od;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-              ev[p] = lo_halves(vr[i][2 * p][w], vr[i][2 * p + 1][w]);
-              od[p] = hi_halves(vr[i][2 * p][w], vr[i][2 * p + 1][w]);
-            }
-            *(u32x4_t*)(dst + (2 * w) * G::kVStride) = ev;
-            *(u32x4_t*)(dst + (2 * w + 1) * G::kVStride) = od;
-          }
-        }
+    for (int i = 0; i < kPer; ++i) {
+      if (live(tid, i)) {
+        const int ch = chunk(tid, i);
+        const int key = ch / kRowChunks, c8 = (ch % kRowChunks) * 8;
+        *(u32x4_t*)(ks + k_lds_row(key) * G::kKStride + c8) = kr[i];
+        if constexpr (kWithV) *(u32x4_t*)(vs + key * G::kVStride + c8) = vr[i];
       }
     }
   }
@@ -166,10 +142,13 @@ struct WaveRows {
       const float mn = grow ? mx : m;
       const float alpha = (mn == m) ? 1.f : fast_exp2(m - mn);
       l *= alpha;
+      // In-place multiply: keeps O in the same registers on both sides of the
+      // branch (a plain `*=` lets the allocator rename O and copy all of it
+      // back on the path that skips the rescale).
 #pragma unroll
       for (int t = 0; t < G::kDTiles; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        for (int r = 0; r < 16; ++r) asm volatile("v_mul_f32 %0, %0, %1" : "+v"(o[t][r]) : "v"(alpha));
       m = mn;
     }
     const float mb = (m == -INFINITY) ? 0.f : m;
@@ -188,12 +167,32 @@ struct WaveRows {
         for (int e = 0; e < 4; ++e)
           pb[2 * t + u][e] = pack_bf16x2(s[t][8 * u + 2 * e], s[t][8 * u + 2 * e + 1]);
     }
-    const uint16_t* a = vt + (lane & 31) * G::kVStride + 8 * (lane >> 5);
+    // A = V^T fragment: lane L needs V[16ks + 8(L/32) + e][32t + L%32], e = 0..7,
+    // fetched as two transpose reads of 4 keys each (see lds_read_tr16).
+    const uint16_t* a = vt + (8 * (lane >> 5) + ((lane >> 2) & 3)) * G::kVStride +
+                        16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int t = 0; t < G::kDTiles; ++t)
-        o[t] = mfma32x32x16(*(const u32x4_t*)(a + (32 * t) * G::kVStride + 16 * ks), pb[ks], o[t]);
+      for (int t = 0; t < G::kDTiles; ++t) {
+        const u32x2_t lo = lds_read_tr16(a + (16 * ks) * G::kVStride + 32 * t);
+        const u32x2_t hi = lds_read_tr16(a + (16 * ks + 4) * G::kVStride + 32 * t);
+        o[t] = mfma32x32x16(u32x4_t{lo[0], lo[1], hi[0], hi[1]}, pb[ks], o[t]);
+      }
+  }
+
+  // One tile: S^T, the causal mask when the tile reaches past this wave's
+  // first query (only ever on diagonal tiles, and only instantiated for
+  // them), online softmax and PV.
+  template <bool kMask>
+  __device__ __forceinline__ void attend(const uint16_t* ks, const uint16_t* vt, int lane,
+                                         float c, int key0, int q0) {
+    f32x16_t s[2];
+    scores(ks, lane, s);
+    if constexpr (kMask) {
+      if (key0 + kKeyTile - 1 > q0) mask(s, key0, q0 + (lane & 31), lane);
+    }
+    softmax_pv(s, vt, lane, c);
   }
 
   // O = O^T / l written as bf16 rows; lse in natural log.
@@ -245,20 +244,27 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
   w.reset();
-  const int ntiles = (qbase + kQT - 1) / kKeyTile + 1;
+  // Tiles 0 .. nfull-1 lie wholly below every query of the group; the last
+  // kQT/64 tiles hold the diagonal and are masked per wave.
+  const uint16_t* Kh = K + hoff;
+  const uint16_t* Vh = V + hoff;
+  const int ntiles = (qbase + kQT) / kKeyTile;
+  const int nfull = qbase / kKeyTile;
   TileStage<D, kNT, true> st;
-  st.load(K + hoff, V + hoff, 0, tid);
-  for (int it = 0; it < ntiles; ++it) {
+  st.load(Kh, Vh, tid);
+  for (int it = 0; it < nfull; ++it) {
     st.store(ks, vt, tid);
     __syncthreads();
-    if (it + 1 < ntiles) st.load(K + hoff, V + hoff, (it + 1) * kKeyTile, tid);
-    const int key0 = it * kKeyTile;
-    if (key0 <= q0) {
-      f32x16_t s[2];
-      w.scores(ks, lane, s);
-      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, q0 + (lane & 31), lane);
-      w.softmax_pv(s, vt, lane, c);
-    }
+    st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
+    w.template attend<false>(ks, vt, lane, c, it * kKeyTile, q0);
+    __syncthreads();
+  }
+  for (int it = nfull; it < ntiles; ++it) {
+    st.store(ks, vt, tid);
+    __syncthreads();
+    if (it + 1 < ntiles)
+      st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
+    if (it * kKeyTile <= q0) w.template attend<true>(ks, vt, lane, c, it * kKeyTile, q0);
     __syncthreads();
   }
   w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
@@ -289,20 +295,21 @@ block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
   const float nl = -lse[(size_t)bh * n + qi] * kLog2e;   // -log2 of the row normaliser
+  const uint16_t* Kh = K + hoff;
   const int ntiles = (qb + 1) * kTPB;
   TileStage<D, kNT, false> st;
-  st.load(K + hoff, nullptr, 0, tid);
+  st.load(Kh, nullptr, tid);
   float blk = 0.f;
   for (int it = 0; it < ntiles; ++it) {
     st.store(ks, nullptr, tid);
     __syncthreads();
-    if (it + 1 < ntiles) st.load(K + hoff, nullptr, (it + 1) * kKeyTile, tid);
+    if (it + 1 < ntiles) st.load(Kh + (size_t)(it + 1) * kKeyTile * D, nullptr, tid);
     const int key0 = it * kKeyTile;
     float part = 0.f;
     if (key0 <= q0) {
       f32x16_t s[2];
       w.scores(ks, lane, s);
-      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, qi, lane);
+      if (it >= qb * kTPB && key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, qi, lane);
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -326,8 +333,10 @@ block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
 
 // ---------------------------------------------------------------------------
 // Block-sparse attention over a CSR support.  One work-group per (batch,
-// head, query block) row, NW = block/32 waves; rows are taken in `order`
-// (longest support first when built by wise_select_support).
+// head, query block) row, NW = block/32 waves.  Schedule slot s (a logical id,
+// contiguous per XCD) runs row order[s]; wise_select_support writes the rows
+// of each head together, longest support first, so an XCD works through a
+// few heads at a time and their K/V tiles stay in its L2.
 // ---------------------------------------------------------------------------
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
@@ -340,17 +349,20 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
   __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
-  const int row = order ? order[blockIdx.x] : (int)blockIdx.x;
+  const int slot = xcd_logical_id();
+  const int row = order ? order[slot] : slot;
   if ((unsigned)row >= (unsigned)rows) return;
   const int bh = row / nb, qb = row % nb;
   const size_t hoff = (size_t)bh * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qb * kB + 32 * wave;
   const int beg = row_ptr[row];
-  const int ntiles = (row_ptr[row + 1] - beg) * kTPB;
+  const int nent = row_ptr[row + 1] - beg;
+  const uint16_t* Kh = K + hoff;
+  const uint16_t* Vh = V + hoff;
 
-  // Tile it -> first key; ids outside 0..qb are ignored (their tile is
-  // neither loaded out of bounds nor used).
+  // Tile it of the row: entry it / kTPB, sub-tile it % kTPB.  Ids outside
+  // 0..qb are skipped (their tile is never loaded out of bounds nor used).
   auto tile_key = [&](int it, bool& ok) {
     const int kb = col_idx[beg + it / kTPB];
     ok = (unsigned)kb <= (unsigned)qb;
@@ -361,21 +373,31 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   w.load_q(Q + hoff, q0, lane);
   w.reset();
   TileStage<D, kNT, true> st;
+  const int ntiles = nent * kTPB;
+  // Entries are ascending, so only the last one can be the diagonal block:
+  // every earlier tile lies wholly below this group's queries.
+  const int nfull = (nent - 1) * kTPB;
   bool ok = false;
   int key0 = ntiles > 0 ? tile_key(0, ok) : 0;
-  if (ntiles > 0) st.load(K + hoff, V + hoff, key0, tid);
-  for (int it = 0; it < ntiles; ++it) {
+  if (ntiles > 0) st.load(Kh + (size_t)key0 * D, Vh + (size_t)key0 * D, tid);
+  for (int it = 0; it < nfull; ++it) {
+    st.store(ks, vt, tid);
+    __syncthreads();
+    bool ok_next;
+    const int key_next = tile_key(it + 1, ok_next);
+    st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
+    if (ok && key0 + kKeyTile - 1 < qb * kB) w.template attend<false>(ks, vt, lane, c, key0, q0);
+    __syncthreads();
+    key0 = key_next;
+    ok = ok_next;
+  }
+  for (int it = max(nfull, 0); it < ntiles; ++it) {
     st.store(ks, vt, tid);
     __syncthreads();
     bool ok_next = false;
     const int key_next = (it + 1 < ntiles) ? tile_key(it + 1, ok_next) : 0;
-    if (it + 1 < ntiles) st.load(K + hoff, V + hoff, key_next, tid);
-    if (ok && key0 <= q0) {
-      f32x16_t s[2];
-      w.scores(ks, lane, s);
-      if (key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, q0 + (lane & 31), lane);
-      w.softmax_pv(s, vt, lane, c);
-    }
+    if (it + 1 < ntiles) st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
+    if (ok && key0 <= q0) w.template attend<true>(ks, vt, lane, c, key0, q0);
     __syncthreads();
     key0 = key_next;
     ok = ok_next;

@@ -13,14 +13,15 @@
 //                        emit a bitmask and a count
 //   scan_kernel          exclusive scan of counts -> row_ptr
 //   scatter_kernel       bitmask -> ascending col_idx
-//   order_*_kernel       stable counting sort of rows by count, descending
+//   order_kernel         per (batch, head): its rows by count descending
+//                        (ties by row id), heads in ascending order
 #include "wise_device.hpp"
 #include "wise_kernels.hpp"
 
 namespace wise {
 
 constexpr int kSelWaves = 4;        // rows per work-group in the per-row kernels
-constexpr int kOrderChunk = 256;    // rows per chunk of the counting sort
+constexpr int kOrderThreads = 256;
 
 // Orderable 32-bit image of a float: unsigned order == float order.
 __device__ __forceinline__ uint32_t float_key(float x) {
@@ -177,64 +178,29 @@ scatter_kernel(const uint64_t* __restrict__ masks, const int32_t* __restrict__ r
   }
 }
 
-// Counting sort of rows by count (descending), stable by row id.
-// (a) per-chunk histograms hist[chunk][c], c = 0..nb
-__global__ void __launch_bounds__(kOrderChunk)
-order_hist_kernel(const int32_t* __restrict__ counts, int rows, int nb, int32_t* __restrict__ hist) {
-  extern __shared__ int32_t h_smem[];
-  for (int c = threadIdx.x; c <= nb; c += kOrderChunk) h_smem[c] = 0;
+// Row order: one work-group per (batch, head).  Row r of the head lands at
+// rank(r) = #{rows with a larger count} + #{earlier rows with the same count}.
+__global__ void __launch_bounds__(kOrderThreads)
+order_kernel(const int32_t* __restrict__ counts, int nb, int32_t* __restrict__ order) {
+  extern __shared__ int32_t o_smem[];
+  const int base = blockIdx.x * nb;
+  for (int r = threadIdx.x; r < nb; r += kOrderThreads) o_smem[r] = counts[base + r];
   __syncthreads();
-  const int r = blockIdx.x * kOrderChunk + threadIdx.x;
-  if (r < rows) atomicAdd(&h_smem[counts[r]], 1);
-  __syncthreads();
-  for (int c = threadIdx.x; c <= nb; c += kOrderChunk)
-    hist[(size_t)blockIdx.x * (nb + 1) + c] = h_smem[c];
-}
-
-// (b) hist[chunk][c] -> rows of count c in earlier chunks; start[c] = rows
-//     with a larger count.
-__global__ void __launch_bounds__(1024)
-order_offsets_kernel(int32_t* __restrict__ hist, int nchunks, int nb, int32_t* __restrict__ start) {
-  for (int c = threadIdx.x; c <= nb; c += 1024) {
-    int run = 0;
-    for (int ch = 0; ch < nchunks; ++ch) {
-      const int h = hist[(size_t)ch * (nb + 1) + c];
-      hist[(size_t)ch * (nb + 1) + c] = run;
-      run += h;
+  for (int r = threadIdx.x; r < nb; r += kOrderThreads) {
+    const int c = o_smem[r];
+    int rank = 0;
+    for (int t = 0; t < nb; ++t) {
+      const int ct = o_smem[t];
+      rank += (ct > c || (ct == c && t < r)) ? 1 : 0;
     }
-    start[c] = run;   // total rows with count c, turned into offsets below
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int c = nb; c >= 0; --c) {
-      const int t = start[c];
-      start[c] = acc;
-      acc += t;
-    }
+    order[base + rank] = base + r;
   }
 }
 
-// (c) place each row.
-__global__ void __launch_bounds__(kOrderChunk)
-order_place_kernel(const int32_t* __restrict__ counts, int rows, int nb,
-                   const int32_t* __restrict__ hist, const int32_t* __restrict__ start,
-                   int32_t* __restrict__ order) {
-  __shared__ int32_t cs[kOrderChunk];
-  const int r = blockIdx.x * kOrderChunk + threadIdx.x;
-  const int c = r < rows ? counts[r] : -1;
-  cs[threadIdx.x] = c;
-  __syncthreads();
-  if (r >= rows) return;
-  int rank = 0;
-  for (int t = 0; t < (int)threadIdx.x; ++t) rank += (cs[t] == c) ? 1 : 0;
-  order[start[c] + hist[(size_t)blockIdx.x * (nb + 1) + c] + rank] = r;
-}
-
-// Workspace layout: counts | masks | hist | start, each 256-B aligned.
+// Workspace layout: counts | masks, each 256-B aligned.
 struct SelectWs {
-  size_t counts, masks, hist, start, total;
-  int words, nchunks;
+  size_t counts, masks, total;
+  int words;
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -243,12 +209,9 @@ static SelectWs select_ws(const Dims& s) {
   SelectWs w;
   const size_t rows = (size_t)s.bh * s.nb;
   w.words = (s.nb + 63) / 64;
-  w.nchunks = (int)((rows + kOrderChunk - 1) / kOrderChunk);
   w.counts = 0;
   w.masks = align256(w.counts + rows * 4);
-  w.hist = align256(w.masks + rows * w.words * 8);
-  w.start = align256(w.hist + (size_t)w.nchunks * (s.nb + 1) * 4);
-  w.total = align256(w.start + (size_t)(s.nb + 1) * 4);
+  w.total = align256(w.masks + rows * w.words * 8);
   return w;
 }
 
@@ -261,8 +224,6 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
   char* base = (char*)ws;
   auto* counts = (int32_t*)(base + w.counts);
   auto* masks = (uint64_t*)(base + w.masks);
-  auto* hist = (int32_t*)(base + w.hist);
-  auto* start = (int32_t*)(base + w.start);
   const int rows = s.bh * s.nb;
   const int groups = (rows + kSelWaves - 1) / kSelWaves;
   const size_t smem = (size_t)kSelWaves * 2 * s.nb * sizeof(uint64_t);
@@ -281,15 +242,9 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, st, counts, rows, row_ptr);
   hipLaunchKernelGGL(scatter_kernel, dim3(groups), dim3(kSelWaves * 64), 0, st, masks, row_ptr,
                      rows, w.words, col_idx);
-  if (row_order != nullptr) {
-    const size_t hsmem = (size_t)(s.nb + 1) * sizeof(int32_t);
-    hipLaunchKernelGGL(order_hist_kernel, dim3(w.nchunks), dim3(kOrderChunk), hsmem, st, counts,
-                       rows, s.nb, hist);
-    hipLaunchKernelGGL(order_offsets_kernel, dim3(1), dim3(1024), 0, st, hist, w.nchunks, s.nb,
-                       start);
-    hipLaunchKernelGGL(order_place_kernel, dim3(w.nchunks), dim3(kOrderChunk), 0, st, counts,
-                       rows, s.nb, hist, start, row_order);
-  }
+  if (row_order != nullptr)
+    hipLaunchKernelGGL(order_kernel, dim3(s.bh), dim3(kOrderThreads), (size_t)s.nb * sizeof(int32_t),
+                       st, counts, s.nb, row_order);
   return hipGetLastError();
 }
 

@@ -14,6 +14,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 constexpr int kKeyTile = 64;    // keys per LDS tile
@@ -27,6 +28,15 @@ constexpr float kLn2 = 0.6931471805599453f;
 __device__ __forceinline__ f32x16_t mfma32x32x16(u32x4_t a, u32x4_t b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// LDS transpose read (ds_read_b64_tr_b16).  Within each 16-lane group g,
+// output lane 16g + i, element j is the 16-bit word at
+// (address supplied by lane 16g + 4j + i/4) + (i % 4).
+__device__ __forceinline__ u32x2_t lds_read_tr16(const uint16_t* p) {
+  auto r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4_t*)(const_cast<uint16_t*>(p)));
+  return __builtin_bit_cast(u32x2_t, r);
 }
 
 // Two fp32 -> packed bf16x2 (round to nearest even), lo in bits 0..15.
@@ -73,11 +83,11 @@ template <int D>
 struct Geo {
   static_assert(D == 64 || D == 96 || D == 128, "head_dim");
   static constexpr int kKStride = D + 8;          // LDS K row stride (bf16): 16 B pad
-  static constexpr int kVStride = kKeyTile + 8;   // LDS V^T row stride (bf16)
+  static constexpr int kVStride = D + 16;         // LDS V row stride (bf16): 32 B pad
   static constexpr int kDChunks = D / 16;         // MFMA k-steps of S^T = K Q^T
   static constexpr int kDTiles = D / 32;          // MFMA m-tiles of O^T = V^T P^T
   static constexpr int kKElems = kKeyTile * kKStride;
-  static constexpr int kVElems = D * kVStride;
+  static constexpr int kVElems = kKeyTile * kVStride;
 };
 
 // Row of the LDS K tile that holds tile-local key `key`.  S^T = K Q^T puts

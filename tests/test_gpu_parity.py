@@ -149,7 +149,7 @@ def test_sparse_random_support(gpu_lib, bt, h, n, d, B):
     nb = n // B
     rng = np.random.default_rng(n * d)
     rp, ci = random_support(None, nb, rng, bt * h)
-    order = O.schedule_order(rp)
+    order = O.schedule_order(rp, nb)
     s = w.make_shape(bt, h, n, d, B)
     o = torch.empty_like(q, device="cuda")
     lse = torch.empty((bt, h, n), device="cuda")
@@ -253,7 +253,7 @@ def test_select_only_parity(gpu_lib, nb, seed):
             nnz = sched.nnz()
             assert np.array_equal(sched.row_ptr.cpu().numpy(), rp_ref), (tau, flags)
             assert np.array_equal(sched.col_idx[:nnz].cpu().numpy(), ci_ref), (tau, flags)
-            assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp_ref))
+            assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp_ref, nb))
 
 
 def test_tiny_trajectory(gpu_lib):

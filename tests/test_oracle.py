@@ -248,9 +248,9 @@ def test_margins_example():
 
 
 def test_schedule_order():
-    rp = np.array([0, 2, 5, 7, 8, 11, 13])
-    order = O.schedule_order(rp)
-    assert list(order) == [1, 4, 0, 2, 5, 3]
+    rp = np.array([0, 2, 5, 7, 8, 11, 13])            # sizes 2 3 2 | 1 3 2
+    assert list(O.schedule_order(rp, 6)) == [1, 4, 0, 2, 5, 3]
+    assert list(O.schedule_order(rp, 3)) == [1, 0, 2, 4, 5, 3]
 
 
 # --------------------------------------------------------------------------
