@@ -153,13 +153,17 @@ struct WaveRows {
     }
     const float mb = (m == -INFINITY) ? 0.f : m;
     u32x4_t pb[4];
+    // The tile's probabilities are summed on their own and added to the row
+    // sum once per tile: a long row (16K keys per lane at 32K) then carries
+    // rounding error ~ tiles * eps instead of ~ keys * eps.
+    float ts = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[t][r], c, -mb));
         s[t][r] = p;
-        l += p;
+        ts += p;
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -169,6 +173,7 @@ struct WaveRows {
     }
     // A = V^T fragment: lane L needs V[16ks + 8(L/32) + e][32t + L%32], e = 0..7,
     // fetched as two transpose reads of 4 keys each (see lds_read_tr16).
+    l += ts;
     const uint16_t* a = vt + (8 * (lane >> 5) + ((lane >> 2) & 3)) * G::kVStride +
                         16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll

@@ -1,0 +1,110 @@
+"""Full-size parity: each workload at its real shape, driven through the same
+pipeline the benchmark times, checked against the CPU oracle on sampled rows
+the oracle computes one by one, and on properties that hold at any size
+(selection on the GPU's own accumulator is bit-exact for every row; the row
+order is the oracle's; accumulator rows sum to the window length)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import wise_oracle as O
+from paper_2609_27373_amd.pipeline import WisePipeline
+from paper_2609_27373_amd.workloads import CONFIGS, Trajectory
+from parity_util import assert_attn, assert_lse, f64, near_tie, say
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_rows(cfg, k=4):
+    bh = cfg.batch * cfg.heads
+    rng = np.random.default_rng(cfg.seed + 17)
+    picks = {(0, cfg.nb - 1), (bh - 1, cfg.nb // 3), (int(rng.integers(bh)), 0),
+             (int(rng.integers(bh)), int(rng.integers(cfg.nb)))}
+    return sorted(picks)[:k]
+
+
+@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k"])
+def test_fullsize_trajectory(gpu_lib, name):
+    cfg = CONFIGS[name]
+    say(f"full-size {name}: B={cfg.batch} H={cfg.heads} n={cfg.seq_len} d={cfg.head_dim} "
+        f"block={cfg.block} t_d={cfg.discovery_steps}")
+    tr = Trajectory(cfg, device="cuda")
+    pipe = WisePipeline.for_config(cfg)
+    rows = sample_rows(cfg)
+    heads = sorted({b for b, _ in rows})
+    keep = {}                                  # sampled heads' inputs (fp32, host) of the steps used
+    need = set(cfg.window) | {cfg.discovery_steps, cfg.discovery_steps + 1}
+    nb, B, d = cfg.nb, cfg.block, cfg.head_dim
+    scale = 1.0 / np.sqrt(d)
+    out = None
+    for t in range(1, cfg.discovery_steps + 2):
+        q, k, v = tr.next(torch.bfloat16)
+        if out is None:
+            out = torch.empty_like(q)
+        flat = [x.view(-1, cfg.seq_len, d) for x in (q, k, v)]
+        if t in need:
+            keep[t] = {h: tuple(x[h].float().cpu() for x in flat) for h in heads}
+        if t <= cfg.discovery_steps:
+            pipe.discovery_step(q, k, v, out, accumulate=t in cfg.window)
+            if t == cfg.discovery_steps:
+                torch.cuda.synchronize()
+                o_last = out.view(-1, cfg.seq_len, d).clone()
+                lse_last = pipe.lse.view(-1, cfg.seq_len).clone()
+                pipe.select()
+        else:
+            lse = torch.empty_like(pipe.lse)
+            pipe.late_step(q, k, v, out, lse)
+    torch.cuda.synchronize()
+    acc = f64(pipe.acc).reshape(-1, nb, nb)
+    sched = pipe.schedule
+    rp = sched.row_ptr.cpu().numpy()
+    ci = sched.col_idx[: int(rp[-1])].cpu().numpy()
+    tau = float(np.float32(cfg.tau))
+
+    # properties over every row
+    np.testing.assert_allclose(acc.sum(-1), len(cfg.window), atol=1e-4)
+    rp_o, ci_o = O.select_support(acc.reshape(cfg.batch, cfg.heads, nb, nb), tau, pipe.flags)
+    assert np.array_equal(rp, rp_o) and np.array_equal(ci, ci_o), "selection on the GPU's acc"
+    assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp, nb))
+    say(f"  density {rp[-1] / (cfg.batch * cfg.heads * nb * (nb + 1) / 2):.4f}, nnz {rp[-1]}")
+
+    # sampled rows against the oracle
+    td = cfg.discovery_steps
+    o_late = out.view(-1, cfg.seq_len, d)
+    lse_late = lse.view(-1, cfg.seq_len)
+    for bh, qb in rows:
+        sl = slice(qb * B, (qb + 1) * B)
+        qh, kh, vh = (x.double().numpy() for x in keep[td][bh])
+        _, o_ref, l_ref = O.causal_attention_rows(qh, kh, vh, np.arange(qb * B, (qb + 1) * B), scale)
+        assert_attn(o_last[bh, sl], o_ref, f"dense row ({bh},{qb})")
+        assert_lse(lse_last[bh, sl], l_ref, f"dense lse ({bh},{qb})")
+        a_ref = sum(O.block_mass_row(keep[t][bh][0].double().numpy(), keep[t][bh][1].double().numpy(),
+                                     qb, B, scale) for t in cfg.window)
+        err = np.abs(acc[bh, qb] - a_ref).max()
+        assert err <= 1e-5 * len(cfg.window), f"acc row ({bh},{qb}): {err:.3g}"
+        want = O.select_row(a_ref, qb, tau, pipe.flags)
+        got = [int(x) for x in ci[rp[bh * nb + qb]:rp[bh * nb + qb + 1]]]
+        if got != want:
+            assert near_tie(a_ref, qb, tau), f"CSR row ({bh},{qb}): gpu {got} oracle {want}"
+            say(f"  near-tie row ({bh},{qb}) reported")
+        ql, kl, vl = (x.double().numpy() for x in keep[td + 1][bh])
+        o_s, l_s = O.sparse_attention_row(ql, kl, vl, qb, got, B, scale)
+        assert_attn(o_late[bh, sl], o_s, f"sparse row ({bh},{qb})")
+        assert_lse(lse_late[bh, sl], l_s, f"sparse lse ({bh},{qb})")
+
+    # the threshold sweep: every tau gives a bit-exact CSR and density grows with tau
+    if len(cfg.taus) > 1:
+        dens = {}
+        for t2 in sorted(cfg.taus):
+            t32 = float(np.float32(t2))
+            sched.select(pipe.acc, t32, pipe.flags)
+            torch.cuda.synchronize()
+            rp2 = sched.row_ptr.cpu().numpy()
+            rp_o2, ci_o2 = O.select_support(acc.reshape(cfg.batch, cfg.heads, nb, nb), t32, pipe.flags)
+            assert np.array_equal(rp2, rp_o2)
+            assert np.array_equal(sched.col_idx[: int(rp2[-1])].cpu().numpy(), ci_o2)
+            dens[t2] = rp2[-1]
+        say(f"  tau sweep nnz: {dens}")
+        vals = [dens[t] for t in sorted(dens)]
+        assert all(a <= b for a, b in zip(vals, vals[1:]))
