@@ -1,10 +1,7 @@
-// attention.hip — the three attention kernels of libwise on gfx950:
+// attention.hip — the two attention kernels of libwise on gfx950:
 //
 //   dense_attn_kernel   causal flash attention, O and natural-log LSE
 //                       (paper Section 3, eq. recurrent_attention)
-//   block_mass_kernel   block-pooled softmax mass acc[qb][kb] += r_qb,kb
-//                       (Section 5.1, eq. block_attention_mass), recomputing
-//                       QK^T against the LSE the dense kernel wrote
 //   sparse_attn_kernel  attention restricted to a CSR block support
 //                       (Section 5.2, eq. wise_attention)
 //
@@ -21,6 +18,9 @@
 // online in base 2 with the exact running max (so the largest probability of
 // a row is exactly 1 in bf16); the O rescale is skipped, wave-uniformly, on
 // tiles that raise no row's max.
+//
+// Work order: see sched_slot (heaviest items of every head first, heads
+// grouped per XCD).
 #include "wise_device.hpp"
 #include "wise_kernels.hpp"
 
@@ -219,14 +219,6 @@ struct WaveRows {
   }
 };
 
-// Work-group id -> logical id such that consecutive logical ids run on the
-// same XCD (hardware deals work-groups round-robin over the 8 XCDs), keeping
-// a head's K/V tiles in one XCD's L2.
-__device__ __forceinline__ int xcd_logical_id() {
-  const int g = gridDim.x, b = blockIdx.x;
-  return (g % 8 == 0) ? (b % 8) * (g / 8) + b / 8 : b;
-}
-
 // ---------------------------------------------------------------------------
 // Dense causal attention.  A work-group of NW waves owns 32*NW consecutive
 // queries of one (batch, head); heavier (later) query tiles are issued first.
@@ -235,13 +227,14 @@ template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-                  float* __restrict__ lse, int n, int qtiles, float c) {
+                  float* __restrict__ lse, int n, int qtiles, int group, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kQT = NW * 32;
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
   __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
-  const int lid = xcd_logical_id();
-  const int bh = lid / qtiles, qt = qtiles - 1 - lid % qtiles;
+  int bh, item;
+  sched_slot(gridDim.x / qtiles, qtiles, group, bh, item);
+  const int qt = qtiles - 1 - item;
   const size_t hoff = (size_t)bh * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
@@ -276,67 +269,6 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
 }
 
 // ---------------------------------------------------------------------------
-// Block mass.  One work-group per (batch, head, query block), NW = block/32
-// waves; the group owns its acc row, so the read-modify-write needs no
-// atomics and the reduction order is fixed.
-// ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
-block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-                  const float* __restrict__ lse, float* __restrict__ acc, int n, int nb,
-                  float c) {
-  using G = Geo<D>;
-  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
-  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
-  __shared__ float red[NW];
-  const int lid = xcd_logical_id();
-  const int bh = lid / nb, qb = nb - 1 - lid % nb;
-  const size_t hoff = (size_t)bh * n * D;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int q0 = qb * kB + 32 * wave;
-  const int qi = q0 + (lane & 31);
-  float* arow = acc + ((size_t)bh * nb + qb) * nb;
-
-  WaveRows<D> w;
-  w.load_q(Q + hoff, q0, lane);
-  const float nl = -lse[(size_t)bh * n + qi] * kLog2e;   // -log2 of the row normaliser
-  const uint16_t* Kh = K + hoff;
-  const int ntiles = (qb + 1) * kTPB;
-  TileStage<D, kNT, false> st;
-  st.load(Kh, nullptr, tid);
-  float blk = 0.f;
-  for (int it = 0; it < ntiles; ++it) {
-    st.store(ks, nullptr, tid);
-    __syncthreads();
-    if (it + 1 < ntiles) st.load(Kh + (size_t)(it + 1) * kKeyTile * D, nullptr, tid);
-    const int key0 = it * kKeyTile;
-    float part = 0.f;
-    if (key0 <= q0) {
-      f32x16_t s[2];
-      w.scores(ks, lane, s);
-      if (it >= qb * kTPB && key0 + kKeyTile - 1 > q0) WaveRows<D>::mask(s, key0, qi, lane);
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) part += fast_exp2(__builtin_fmaf(s[t][r], c, nl));
-    }
-    blk += wave_sum(part);
-    const bool last = (it % kTPB) == kTPB - 1;
-    if (last && lane == 0) red[wave] = blk;
-    __syncthreads();
-    if (last) {
-      if (tid == 0) {
-        float tot = 0.f;
-#pragma unroll
-        for (int i = 0; i < NW; ++i) tot += red[i];
-        arow[it / kTPB] += tot * (1.f / kB);
-      }
-      blk = 0.f;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Block-sparse attention over a CSR support.  One work-group per (batch,
 // head, query block) row, NW = block/32 waves.  Schedule slot s (a logical id,
 // contiguous per XCD) runs row order[s]; wise_select_support writes the rows
@@ -349,13 +281,14 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
                    const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
                    uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
-                   float c) {
+                   int group, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
   __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
-  const int slot = xcd_logical_id();
-  const int row = order ? order[slot] : slot;
+  int sh, sit;
+  sched_slot(gridDim.x / nb, nb, group, sh, sit);
+  const int row = order ? order[sh * nb + sit] : sh * nb + (nb - 1 - sit);
   if ((unsigned)row >= (unsigned)rows) return;
   const int bh = row / nb, qb = row % nb;
   const size_t hoff = (size_t)bh * n * D;
@@ -423,11 +356,11 @@ static hipError_t launch_dense_d(const Dims& s, const void* q, const void* k, co
   if (s.n % 128 == 0) {
     const int qt = s.n / 128;
     hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(s.bh * qt), dim3(256), 0, st, Q, K, V,
-                       (uint16_t*)o, lse, s.n, qt, c);
+                       (uint16_t*)o, lse, s.n, qt, sched_group(s.bh), c);
   } else {
     const int qt = s.n / 64;
     hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(s.bh * qt), dim3(128), 0, st, Q, K, V,
-                       (uint16_t*)o, lse, s.n, qt, c);
+                       (uint16_t*)o, lse, s.n, qt, sched_group(s.bh), c);
   }
   return hipGetLastError();
 }
@@ -442,30 +375,6 @@ hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void*
 }
 
 template <int D>
-static hipError_t launch_mass_d(const Dims& s, const void* q, const void* k, const float* lse,
-                                float* acc, hipStream_t st) {
-  const float c = s.scale * kLog2e;
-  const auto* Q = (const uint16_t*)q;
-  const auto* K = (const uint16_t*)k;
-  if (s.block == 64)
-    hipLaunchKernelGGL((block_mass_kernel<D, 2>), dim3(s.bh * s.nb), dim3(128), 0, st, Q, K, lse,
-                       acc, s.n, s.nb, c);
-  else
-    hipLaunchKernelGGL((block_mass_kernel<D, 4>), dim3(s.bh * s.nb), dim3(256), 0, st, Q, K, lse,
-                       acc, s.n, s.nb, c);
-  return hipGetLastError();
-}
-
-hipError_t launch_mass(const Dims& s, const void* q, const void* k, const float* lse, float* acc,
-                       hipStream_t st) {
-  switch (s.d) {
-    case 64: return launch_mass_d<64>(s, q, k, lse, acc, st);
-    case 96: return launch_mass_d<96>(s, q, k, lse, acc, st);
-    default: return launch_mass_d<128>(s, q, k, lse, acc, st);
-  }
-}
-
-template <int D>
 static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, const void* v,
                                   const int32_t* rp, const int32_t* ci, const int32_t* order,
                                   void* o, float* lse, hipStream_t st) {
@@ -476,10 +385,12 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const int rows = s.bh * s.nb;
   if (s.block == 64)
     hipLaunchKernelGGL((sparse_attn_kernel<D, 2>), dim3(rows), dim3(128), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, c);
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh),
+                       c);
   else
     hipLaunchKernelGGL((sparse_attn_kernel<D, 4>), dim3(rows), dim3(256), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, c);
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh),
+                       c);
   return hipGetLastError();
 }
 
