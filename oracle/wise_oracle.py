@@ -16,6 +16,17 @@ fusion or reordering beyond what the definition states:
                           set, plus forced sink / diagonal blocks
   select_support_union    Section 5.1, eq. (block_working_set), the paper's
                           temporal union of per-step supports
+  step_supports           the per-step sets B_q^(t, eta) inside that union
+  rolling_working_set     Appendix C, "Stability of the Deployed Working Set":
+                          W_q^(t), the union over steps max(1, t-3)..t
+  overlap_counts, jaccard the adjacent rolling-set Jaccard J_roll of the same
+                          subsection, as |A & B| and |A | B| over all
+                          (batch, head, query block, key block) memberships
+  retained_mass           Section 7.1 and Appendix B (evaluation metrics):
+                          the fraction of unrestricted full-attention mass of
+                          a step that falls inside a support, from the
+                          attention probabilities themselves
+  support_block_mass      the same quantity from block masses, per row
   schedule_order          per-head longest-support-first ordering of CSR rows
   sparse_attention        Section 5.2, eq. (wise_attention), gather form
   sparse_attention_masked Section 5.2, eq. (wise_attention) with the mask R
@@ -198,6 +209,89 @@ def select_support_union(step_masses, tau, flags=FORCE_SINK | FORCE_DIAG):
                 col_idx.extend(sorted(u))
                 row_ptr.append(len(col_idx))
     return np.asarray(row_ptr, dtype=np.int32), np.asarray(col_idx, dtype=np.int32)
+
+
+def step_supports(step_mass, tau):
+    """B_q^(t, eta) of one step for every row (no forced blocks): list over
+    rows r = (b*heads + h)*nb + qb of sorted block-id lists."""
+    r = _f64(step_mass)
+    bt, h, nb, _ = r.shape
+    flat = r.reshape(bt * h * nb, nb)
+    return [select_row(flat[i], i % nb, tau, flags=0) for i in range(bt * h * nb)]
+
+
+def csr_rows(row_ptr, col_idx):
+    """CSR -> list over rows of block-id lists."""
+    return [[int(x) for x in col_idx[row_ptr[i]:row_ptr[i + 1]]] for i in range(len(row_ptr) - 1)]
+
+
+def rolling_working_set(per_step, t, width=4):
+    """W_q^(t) = union of B_q^(s) for s = max(1, t - width + 1) .. t.
+
+    per_step[s - 1] is step s's support (list over rows of block-id lists,
+    as from step_supports); returns a list over rows of sorted lists."""
+    lo = max(1, t - width + 1)
+    rows = len(per_step[0])
+    out = []
+    for i in range(rows):
+        u = set()
+        for s in range(lo, t + 1):
+            u.update(per_step[s - 1][i])
+        out.append(sorted(u))
+    return out
+
+
+def overlap_counts(a_rows, b_rows):
+    """(|A & B|, |A | B|) of two supports read as sets of (row, key block)."""
+    inter = union = 0
+    for x, y in zip(a_rows, b_rows):
+        x, y = set(x), set(y)
+        inter += len(x & y)
+        union += len(x | y)
+    return inter, union
+
+
+def jaccard(a_rows, b_rows):
+    """|A & B| / |A | B| over (row, key block) memberships (1 for two empty sets)."""
+    i, u = overlap_counts(a_rows, b_rows)
+    return 1.0 if u == 0 else i / u
+
+
+def retained_mass(q, k, row_ptr, col_idx, block, scale=None):
+    """Fraction of the unrestricted causal attention mass of one step that
+    lies inside a block support: sum of A_ij over causal (i, j) with
+    b(j) in B_{q(i)}, over the sum of A_ij over all causal (i, j) (= n per
+    head).  Returns (per-head fractions [bt][h], overall fraction)."""
+    q, k = _f64(q), _f64(k)
+    bt, h, n, d = q.shape
+    scale = default_scale(d) if scale is None else float(scale)
+    allowed = working_set_mask(row_ptr, col_idx, n, block, bt, h)
+    causal = np.tril(np.ones((n, n), dtype=bool))
+    inside = np.zeros((bt, h))
+    total = np.zeros((bt, h))
+    for b in range(bt):
+        for hh in range(h):
+            s = np.where(causal, (q[b, hh] @ k[b, hh].T) * scale, -np.inf)
+            a = np.exp(s - s.max(axis=1, keepdims=True))
+            a /= a.sum(axis=1, keepdims=True)
+            inside[b, hh] = a[allowed[b, hh] & causal].sum()
+            total[b, hh] = a.sum()
+    return inside / total, inside.sum() / total.sum()
+
+
+def support_block_mass(step_mass, row_ptr, col_idx):
+    """Per row (b, h, qb): (sum of r_{qb,kb} over kb in the row's support,
+    sum of r_{qb,kb} over kb <= qb), from one step's block masses."""
+    r = _f64(step_mass)
+    bt, h, nb, _ = r.shape
+    flat = r.reshape(bt * h * nb, nb)
+    out = np.zeros((bt * h * nb, 2))
+    for i in range(bt * h * nb):
+        qb = i % nb
+        blocks = [int(x) for x in col_idx[row_ptr[i]:row_ptr[i + 1]] if 0 <= x <= qb]
+        out[i, 0] = flat[i, blocks].sum()
+        out[i, 1] = flat[i, :qb + 1].sum()
+    return out
 
 
 def schedule_order(row_ptr, nb):

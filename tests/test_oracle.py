@@ -240,6 +240,112 @@ def test_union_differs_from_accumulated_mass():
     assert list(ci_a[rp_a[3]:rp_a[4]]) == [0, 1, 2]
 
 
+def _random_masses(bt, h, nb, seed, steps=1):
+    """Per-step block masses: positive causal rows summing to 1."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(steps):
+        r = rng.gamma(0.3, size=(bt, h, nb, nb)) * np.tril(np.ones((nb, nb)))
+        out.append(r / r.sum(-1, keepdims=True))
+    return out
+
+
+def test_union_of_identical_steps_is_single_selection():
+    """Every step the same: the union equals one step's selection, forced
+    blocks included."""
+    (r,) = _random_masses(2, 2, 9, 3)
+    for flags in (0, O.FORCE_SINK, O.FORCE_SINK | O.FORCE_DIAG):
+        rp_u, ci_u = O.select_support_union([r, r, r, r], 0.9, flags)
+        rp_s, ci_s = O.select_support(r, 0.9, flags)
+        assert np.array_equal(rp_u, rp_s) and np.array_equal(ci_u, ci_s)
+
+
+def test_union_contains_every_step_and_nothing_else():
+    ms = _random_masses(1, 3, 12, 4, steps=4)
+    rp, ci = O.select_support_union(ms, 0.95, flags=O.FORCE_SINK)
+    rows = O.csr_rows(rp, ci)
+    steps = [O.step_supports(m, 0.95) for m in ms]
+    for i, row in enumerate(rows):
+        members = set().union(*(set(st[i]) for st in steps)) | {0}
+        assert row == sorted(members)
+        # each per-step set meets its own threshold (eq. block_working_set)
+        for m, st in zip(ms, steps):
+            v = m.reshape(-1, 12)[i]
+            assert v[st[i]].sum() >= 0.95 * v[: i % 12 + 1].sum()
+
+
+def test_rolling_working_set_by_hand():
+    """W^(t) = union of the last min(t, 4) per-step sets; one row, 6 steps."""
+    per_step = [[[1]], [[2]], [[1, 3]], [[4]], [[5]], [[6]]]
+    want = {1: [1], 2: [1, 2], 3: [1, 2, 3], 4: [1, 2, 3, 4], 5: [1, 2, 3, 4, 5],
+            6: [1, 3, 4, 5, 6]}
+    for t, w in want.items():
+        assert O.rolling_working_set(per_step, t) == [w]
+    assert O.rolling_working_set(per_step, 6, width=1) == [[6]]
+
+
+def test_jaccard_by_hand():
+    a = [[0, 1], [2], []]
+    b = [[1, 2], [2], [0]]
+    assert O.overlap_counts(a, b) == (2, 5)                 # {1} + {2}; {0,1,2} + {2} + {0}
+    assert O.jaccard(a, b) == 2 / 5
+    assert O.jaccard(a, a) == 1.0 and O.jaccard([[]], [[]]) == 1.0
+    assert O.jaccard([[0]], [[1]]) == 0.0
+    assert O.jaccard([[0, 1]], [[0, 1, 2, 3]]) == 0.5       # nested: |A| / |B|
+
+
+def _uniform_retained(n, B, blocks_of):
+    """Q = 0: A_ij = 1/(i+1) over j <= i, so the mass of query i inside its
+    support is (number of admitted keys j <= i) / (i + 1); exact rationals."""
+    tot = Fraction(0)
+    for i in range(n):
+        keys = sum(min(B, max(0, i + 1 - kb * B)) for kb in blocks_of(i // B))
+        tot += Fraction(keys, i + 1)
+    return tot / n
+
+
+@pytest.mark.parametrize("n,B", [(256, 64), (192, 32)])
+def test_retained_mass_uniform_closed_form(n, B):
+    nb = n // B
+    k = rnd((1, 1, n, 4), n)
+    q = np.zeros((1, 1, n, 4))
+    cases = {"full": lambda qb: range(qb + 1), "diag": lambda qb: [qb], "sink": lambda qb: [0],
+             "sink+diag": lambda qb: sorted({0, qb})}
+    for name, blocks_of in cases.items():
+        rp, ci = [0], []
+        for qb in range(nb):
+            ci.extend(blocks_of(qb))
+            rp.append(len(ci))
+        rp, ci = np.array(rp), np.array(ci)
+        per_head, frac = O.retained_mass(q, k, rp, ci, B)
+        want = float(_uniform_retained(n, B, blocks_of))
+        assert abs(frac - want) < 1e-13, (name, frac, want)
+        assert abs(per_head[0, 0] - want) < 1e-13
+        # block-mass route: the same fraction from r (rows of r sum to 1)
+        bm = O.support_block_mass(O.block_mass(q, k, B), rp, ci)
+        assert abs(bm[:, 0].sum() / bm[:, 1].sum() - want) < 1e-13, name
+        if name == "full":
+            assert frac == pytest.approx(1.0, abs=1e-14)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_retained_mass_two_routes_agree(seed):
+    """From the probabilities and from block masses, on random logits and a
+    selected support; the support of the same step keeps at least tau of
+    every row's mass."""
+    q, k = rnd((2, 2, 2, 256, 16), seed, 1.5)
+    B, tau = 32, 0.9
+    r = O.block_mass(q, k, B)
+    rp, ci = O.select_support(r, tau, flags=0)
+    per_head, frac = O.retained_mass(q, k, rp, ci, B)
+    bm = O.support_block_mass(r, rp, ci)
+    assert np.all(bm[:, 0] >= tau * bm[:, 1] - 1e-15)
+    assert abs(bm[:, 0].sum() / bm[:, 1].sum() - frac) < 1e-12
+    np.testing.assert_allclose(bm[:, 1], 1.0, atol=1e-12)
+    hp = bm[:, 0].reshape(2, 2, -1).sum(-1) / bm[:, 1].reshape(2, 2, -1).sum(-1)
+    np.testing.assert_allclose(hp, per_head, atol=1e-12)
+
+
 def test_margins_example():
     m = O.support_margins(np.array([0.1, 0.6, 0.3]), 2, 0.8)
     assert m["kstar"] == 2
