@@ -32,7 +32,7 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2609_27373_amd import metrics, wise  # noqa: E402
+from paper_2609_27373_amd import diagnostics, metrics, wise  # noqa: E402
 from paper_2609_27373_amd.pipeline import WisePipeline  # noqa: E402
 from paper_2609_27373_amd.workloads import CONFIGS, Trajectory  # noqa: E402
 
@@ -124,9 +124,26 @@ def dense_on_late(cfg, pipe, steps, out, timer):
         timer.stop(e, "dense")
 
 
-def measure(cfg, K, W, tau=None):
+def diagnose(cfg, pipe, steps):
+    """Routing diagnostics of the trajectory just timed (outside any timed
+    region): retained future full-attention mass of the frozen support on
+    every late step, and the rolling working-set stability."""
+    scratch = (torch.empty_like(steps[0][0]), torch.empty_like(pipe.lse),
+               torch.empty_like(pipe.acc))
+    fr = [diagnostics.retained_mass(pipe.shape, *steps[t - 1], pipe.schedule, scratch)[0]
+          for t in range(cfg.discovery_steps + 1, cfg.steps + 1)]
+    st = diagnostics.rolling_stability(pipe.shape, steps, pipe.tau, cfg.discovery_steps)
+    jr = st["j_roll"]
+    return {"retained_future_mass_mean": float(np.mean(fr)),
+            "retained_future_mass_min": float(np.min(fr)),
+            "j_roll_at_td": jr.get(cfg.discovery_steps),
+            "j_roll_mean_late": float(np.mean([jr[t] for t in jr if t > cfg.discovery_steps])),
+            "j_td_T": st["j_td_T"]}
+
+
+def measure(cfg, K, W, tau=None, mode="accumulate", diag=False):
     steps = make_inputs(cfg)
-    pipe = WisePipeline.for_config(cfg, tau=tau)
+    pipe = WisePipeline.for_config(cfg, tau=tau, mode=mode)
     out = torch.empty_like(steps[0][0])
     for _ in range(W):
         trajectory(cfg, pipe, steps, out)
@@ -157,7 +174,7 @@ def measure(cfg, K, W, tau=None):
     L = cfg.late_steps
     late_ms, dense_ms, sel_ms = float(np.median(late)), float(np.median(dense)), float(np.median(sel))
     res = dict(
-        workload=cfg.name, tau=float(tau if tau is not None else cfg.tau),
+        workload=cfg.name, mode=mode, tau=float(tau if tau is not None else cfg.tau),
         density=metrics.density(rp, cfg.nb, bh), nnz=int(rp[-1]),
         late_ms=late_ms, late_ms_mean=float(late.mean()),
         late_ms_iqr=[float(np.percentile(late, 25)), float(np.percentile(late, 75))],
@@ -170,6 +187,8 @@ def measure(cfg, K, W, tau=None):
         speedup_trajectory=(cfg.steps * dense_ms) / (float(np.median(disc)) + sel_ms + L * late_ms),
         trajectory_ms_wall=wall,
     )
+    if diag:
+        res.update(diagnose(cfg, pipe, steps))
     del steps
     torch.cuda.empty_cache()
     return res
@@ -225,6 +244,8 @@ def main():
     ap.add_argument("--config", default="4k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-regime", action="store_true")
+    ap.add_argument("--no-diagnostics", action="store_true",
+                    help="skip the retained-mass / rolling-stability diagnostics")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a "
                          "known-size reference for hardware byte counters)")
@@ -246,12 +267,15 @@ def main():
         del src, dst
     cfg = CONFIGS[args.config]
     log(f"[bench] {cfg.name}: generating {cfg.steps} steps of inputs")
-    main_res = measure(cfg, args.steps, args.warmup)
+    main_res = measure(cfg, args.steps, args.warmup, diag=not args.no_diagnostics)
     log(f"[bench] {json.dumps(main_res)}")
-    pr = None
+    pr = pu = None
     if not args.no_paper_regime and args.config == "4k":
-        pr = measure(CONFIGS["4k-pr"], args.steps, args.warmup)
+        pr = measure(CONFIGS["4k-pr"], args.steps, args.warmup, diag=not args.no_diagnostics)
         log(f"[bench] paper-regime {json.dumps(pr)}")
+        pu = measure(CONFIGS["4k-pr"], args.steps, args.warmup, mode="union",
+                     diag=not args.no_diagnostics)
+        log(f"[bench] paper-regime, union of per-step supports {json.dumps(pu)}")
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -290,6 +314,8 @@ def main():
         "detail": {k: (round(v, 5) if isinstance(v, float) else v) for k, v in main_res.items()},
         "paper_regime": None if pr is None else {
             k: (round(v, 5) if isinstance(v, float) else v) for k, v in pr.items()},
+        "paper_regime_union": None if pu is None else {
+            k: (round(v, 5) if isinstance(v, float) else v) for k, v in pu.items()},
         "context": "paper: up to 1.76x late-step speedup over FlashAttention at 4K on an RTX A6000",
     }
     print(json.dumps(line), flush=True)

@@ -30,9 +30,16 @@
  *  - Calls are stateless and re-entrant; calls on different streams with
  *    disjoint outputs may run concurrently.  No C++ exception crosses the ABI.
  *  - Supported: head_dim in {64, 96, 128}; block in {64, 128};
- *    seq_len % block == 0; nb <= 1024 for wise_select_support.
- *  - Alignment: q, k, v, o 16 bytes; workspace 256 bytes; every other
- *    pointer 4 bytes.  A misaligned pointer is WISE_ERR_SHAPE.
+ *    seq_len % block == 0; nb <= 1024 for wise_select_support,
+ *    wise_select_step and wise_support_from_masks.
+ *  - Support bitmasks (the union mode and the diagnostics): uint64
+ *    [rows][words], words = wise_mask_words(s) = ceil(nb / 64); bit
+ *    (kb & 63) of word kb >> 6 of row r is set iff key block kb belongs to
+ *    that row's set.  Several masks "back to back" means mask i starts at
+ *    element i * rows * words.
+ *  - Alignment: q, k, v, o 16 bytes; workspace 256 bytes; masks, counts
+ *    and fp64 arrays 8 bytes; every other pointer 4 bytes.  A misaligned
+ *    pointer is WISE_ERR_SHAPE.
  */
 #ifndef WISE_H
 #define WISE_H
@@ -44,7 +51,7 @@
 extern "C" {
 #endif
 
-#define WISE_ABI_VERSION 1
+#define WISE_ABI_VERSION 2
 
 typedef enum {
   WISE_OK = 0,
@@ -166,6 +173,102 @@ wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k,
                              const void* v, const int32_t* row_ptr,
                              const int32_t* col_idx, const int32_t* row_order,
                              void* o, float* lse, void* hip_stream);
+
+/*
+ * wise_select_step — one discovery step's own support B_q^(t, eta), the set
+ * that the paper's temporal union collects (Section 5.1, eq.
+ * "block_working_set"), as a bitmask.
+ *
+ * Per row, steps 1-4 of wise_select_support on that step's masses with no
+ * forced blocks (flags = 0): the heaviest k* blocks, k* the first prefix of
+ * the (mass desc, block asc) order whose fp64 sum reaches tau of the row
+ * total; an empty set (row total 0) becomes {qb}.
+ *
+ *   r     : fp32 [batch][heads][nb][nb], read-only: ONE step's block masses
+ *           (wise_dense_attn_accum pooling into a zeroed buffer gives them).
+ *   tau   : 0 < tau <= 1.
+ *   mask  : uint64 [rows][words], every word written.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_RANGE,
+ *         WISE_ERR_HIP.
+ */
+wise_status wise_select_step(const wise_shape* s, const float* r, float tau,
+                             uint64_t* mask, void* hip_stream);
+
+/*
+ * wise_support_from_masks — the paper's working set of Section 5.1, eq.
+ * "block_working_set": per row, the union of n_masks per-step sets (masks
+ * back to back, e.g. the window steps t_d-3..t_d from wise_select_step),
+ * plus the blocks named in `flags`, emitted as CSR and row order exactly as
+ * wise_select_support emits them.  Bits of key blocks past the diagonal are
+ * ignored; an empty union with flags = 0 becomes {qb}.
+ *
+ *   masks     : uint64 [n_masks][rows][words], read-only.  n_masks >= 1.
+ *   flags, row_ptr, col_idx, row_order, workspace, workspace_bytes: as for
+ *               wise_select_support (same workspace size).
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE (also n_masks < 1),
+ *         WISE_ERR_UNSUPPORTED, WISE_ERR_RANGE, WISE_ERR_WORKSPACE, WISE_ERR_HIP.
+ */
+wise_status wise_support_from_masks(const wise_shape* s, const uint64_t* masks,
+                                    int32_t n_masks, uint32_t flags,
+                                    int32_t* row_ptr, int32_t* col_idx,
+                                    int32_t* row_order, void* workspace,
+                                    size_t workspace_bytes, void* hip_stream);
+
+/*
+ * wise_mask_union — out = bitwise OR of n_masks masks stored back to back:
+ * the rolling working set W_q^(t) of Appendix C ("Stability of the Deployed
+ * Working Set") when the masks are the per-step sets of steps
+ * max(1, t-3)..t.
+ *
+ *   masks : uint64 [n_masks][rows][words], read-only.  n_masks >= 1.
+ *   out   : uint64 [rows][words], written; it may coincide with one of the
+ *           masks (each word is read before it is written), any other
+ *           overlap is undefined.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE (also n_masks < 1), WISE_ERR_HIP.
+ */
+wise_status wise_mask_union(const wise_shape* s, const uint64_t* masks,
+                            int32_t n_masks, uint64_t* out, void* hip_stream);
+
+/*
+ * wise_mask_overlap — sizes of the intersection and union of two masks read
+ * as sets of (row, key block): counts[0] = |A & B|, counts[1] = |A | B|.
+ * Their ratio is the adjacent rolling-set Jaccard J_roll of Appendix C
+ * ("Stability of the Deployed Working Set") for A = W^(t-1), B = W^(t).
+ *
+ *   a, b   : uint64 [rows][words], read-only.
+ *   counts : int64 [2], device, written.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_HIP.
+ */
+wise_status wise_mask_overlap(const wise_shape* s, const uint64_t* a,
+                              const uint64_t* b, int64_t* counts,
+                              void* hip_stream);
+
+/*
+ * wise_support_mass — attention mass a block support retains from one step
+ * of unrestricted attention: the retained future full-attention mass of
+ * Section 7.1 and Appendix B (evaluation metrics), computed from that step's
+ * block masses r (eq. "block_attention_mass").  Since each query's
+ * probabilities sum to 1, sum_rows inside / sum_rows total is the fraction
+ * of all causal attention mass that falls inside the support.
+ *
+ *   r        : fp32 [batch][heads][nb][nb], read-only: one step's masses.
+ *   row_ptr, col_idx : a CSR support as for wise_sparse_attn (ids outside
+ *              0..qb are skipped).
+ *   row_mass : fp64 [rows][2], written: (sum of r[row][kb] over the row's
+ *              blocks, sum of r[row][kb] over kb <= qb), each summed in fp64
+ *              in a fixed order (bitwise reproducible).
+ *   totals   : fp64 [2] or NULL, written: the two columns of row_mass summed
+ *              over all rows, in a fixed order.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_HIP.
+ */
+wise_status wise_support_mass(const wise_shape* s, const float* r,
+                              const int32_t* row_ptr, const int32_t* col_idx,
+                              double* row_mass, double* totals,
+                              void* hip_stream);
+
+/* 64-bit words per row of a support bitmask: ceil(nb / 64)
+ * (-1 for an invalid shape). */
+int32_t wise_mask_words(const wise_shape* s);
 
 /* Bytes of device workspace wise_select_support needs for shape s
  * (0 for an invalid shape). */

@@ -15,6 +15,17 @@
 //   scatter_kernel       bitmask -> ascending col_idx
 //   order_kernel         per (batch, head): its rows by count descending
 //                        (ties by row id), heads in ascending order
+//
+// The paper's own working set (Section 5.1, eq. block_working_set) is the
+// union over the discovery window of per-step sets B_q^(t, eta).  For it the
+// per-row kernel runs on one step's masses with no forced blocks and leaves
+// the step's bitmask with the caller; union_rows_kernel ORs any number of
+// such masks, adds the forced blocks, and feeds the same scan / scatter /
+// order kernels.  Two diagnostics close the file: the (intersection, union)
+// sizes of two masks (the adjacent rolling-set Jaccard of Appendix C,
+// "Stability of the Deployed Working Set") and the attention mass a support
+// retains from one step's block masses (Section 7.1 and Appendix B, the
+// retained future full-attention mass).
 #include "wise_device.hpp"
 #include "wise_kernels.hpp"
 
@@ -108,7 +119,7 @@ select_rows_kernel(const float* __restrict__ acc, int rows, int nb, double tau, 
     total = 1;
   }
   if (active && lane == 0) {
-    counts[row] = total;
+    if (counts != nullptr) counts[row] = total;
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (e < words) masks[(size_t)row * words + e] = mword[e];
@@ -205,10 +216,12 @@ struct SelectWs {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+int mask_words(const Dims& s) { return (s.nb + 63) / 64; }
+
 static SelectWs select_ws(const Dims& s) {
   SelectWs w;
   const size_t rows = (size_t)s.bh * s.nb;
-  w.words = (s.nb + 63) / 64;
+  w.words = mask_words(s);
   w.counts = 0;
   w.masks = align256(w.counts + rows * 4);
   w.total = align256(w.masks + rows * w.words * 8);
@@ -217,6 +230,39 @@ static SelectWs select_ws(const Dims& s) {
 
 size_t select_workspace_bytes(const Dims& s) { return select_ws(s).total; }
 
+// Per-row selection of every row: counts (may be null) and bitmasks.
+static void launch_rows(const Dims& s, const float* acc, float tau, uint32_t flags,
+                        int32_t* counts, uint64_t* masks, hipStream_t st) {
+  const int rows = s.bh * s.nb, words = mask_words(s);
+  const int groups = (rows + kSelWaves - 1) / kSelWaves;
+  const size_t smem = (size_t)kSelWaves * 2 * s.nb * sizeof(uint64_t);
+  const dim3 sg(groups), sb(kSelWaves * 64);
+  const double dtau = (double)tau;
+  if (s.nb <= 64)
+    hipLaunchKernelGGL(select_rows_kernel<1>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, words);
+  else if (s.nb <= 128)
+    hipLaunchKernelGGL(select_rows_kernel<2>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, words);
+  else if (s.nb <= 256)
+    hipLaunchKernelGGL(select_rows_kernel<4>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, words);
+  else if (s.nb <= 512)
+    hipLaunchKernelGGL(select_rows_kernel<8>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, words);
+  else
+    hipLaunchKernelGGL(select_rows_kernel<16>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, words);
+}
+
+// counts + masks (in the workspace) -> row_ptr, col_idx, row_order.
+static void launch_csr(const Dims& s, const int32_t* counts, const uint64_t* masks,
+                       int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, hipStream_t st) {
+  const int rows = s.bh * s.nb;
+  const int groups = (rows + kSelWaves - 1) / kSelWaves;
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, st, counts, rows, row_ptr);
+  hipLaunchKernelGGL(scatter_kernel, dim3(groups), dim3(kSelWaves * 64), 0, st, masks, row_ptr,
+                     rows, mask_words(s), col_idx);
+  if (row_order != nullptr)
+    hipLaunchKernelGGL(order_kernel, dim3(s.bh), dim3(kOrderThreads), (size_t)s.nb * sizeof(int32_t),
+                       st, counts, s.nb, row_order);
+}
+
 hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t flags,
                          int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, void* ws,
                          hipStream_t st) {
@@ -224,27 +270,187 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
   char* base = (char*)ws;
   auto* counts = (int32_t*)(base + w.counts);
   auto* masks = (uint64_t*)(base + w.masks);
+  launch_rows(s, acc, tau, flags, counts, masks, st);
+  launch_csr(s, counts, masks, row_ptr, col_idx, row_order, st);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Temporal union of per-step supports
+// ---------------------------------------------------------------------------
+
+hipError_t launch_select_step(const Dims& s, const float* r, float tau, uint64_t* mask,
+                              hipStream_t st) {
+  launch_rows(s, r, tau, 0u, nullptr, mask, st);
+  return hipGetLastError();
+}
+
+constexpr int kMaskThreads = 256;
+
+// One thread per row: OR of the row's words over every mask, bits past the
+// diagonal dropped, forced blocks added, an empty row given its diagonal.
+__global__ void __launch_bounds__(kMaskThreads)
+union_rows_kernel(const uint64_t* __restrict__ masks, int n_masks, size_t slab, int rows, int nb,
+                  int words, uint32_t flags, int32_t* __restrict__ counts,
+                  uint64_t* __restrict__ out) {
+  const int row = blockIdx.x * kMaskThreads + threadIdx.x;
+  if (row >= rows) return;
+  const int qb = row % nb;
+  const size_t base = (size_t)row * words;
+  int total = 0;
+  for (int w = 0; w < words; ++w) {
+    uint64_t m = 0;
+    for (int i = 0; i < n_masks; ++i) m |= masks[(size_t)i * slab + base + w];
+    const int lo = 64 * w;
+    const uint64_t keep = qb < lo ? 0ull : (qb - lo >= 63 ? ~0ull : (~0ull >> (63 - (qb - lo))));
+    m &= keep;
+    if (w == 0 && (flags & 1u)) m |= 1ull;
+    if (w == (qb >> 6) && (flags & 2u)) m |= 1ull << (qb & 63);
+    out[base + w] = m;
+    total += __builtin_popcountll(m);
+  }
+  if (total == 0) {
+    out[base + (qb >> 6)] = 1ull << (qb & 63);
+    total = 1;
+  }
+  counts[row] = total;
+}
+
+hipError_t launch_support_from_masks(const Dims& s, const uint64_t* masks, int n_masks,
+                                     uint32_t flags, int32_t* row_ptr, int32_t* col_idx,
+                                     int32_t* row_order, void* ws, hipStream_t st) {
+  const SelectWs w = select_ws(s);
+  char* base = (char*)ws;
+  auto* counts = (int32_t*)(base + w.counts);
+  auto* umask = (uint64_t*)(base + w.masks);
   const int rows = s.bh * s.nb;
-  const int groups = (rows + kSelWaves - 1) / kSelWaves;
-  const size_t smem = (size_t)kSelWaves * 2 * s.nb * sizeof(uint64_t);
-  const dim3 sg(groups), sb(kSelWaves * 64);
-  const double dtau = (double)tau;
-  if (s.nb <= 64)
-    hipLaunchKernelGGL(select_rows_kernel<1>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
-  else if (s.nb <= 128)
-    hipLaunchKernelGGL(select_rows_kernel<2>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
-  else if (s.nb <= 256)
-    hipLaunchKernelGGL(select_rows_kernel<4>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
-  else if (s.nb <= 512)
-    hipLaunchKernelGGL(select_rows_kernel<8>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
-  else
-    hipLaunchKernelGGL(select_rows_kernel<16>, sg, sb, smem, st, acc, rows, s.nb, dtau, flags, counts, masks, w.words);
-  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, st, counts, rows, row_ptr);
-  hipLaunchKernelGGL(scatter_kernel, dim3(groups), dim3(kSelWaves * 64), 0, st, masks, row_ptr,
-                     rows, w.words, col_idx);
-  if (row_order != nullptr)
-    hipLaunchKernelGGL(order_kernel, dim3(s.bh), dim3(kOrderThreads), (size_t)s.nb * sizeof(int32_t),
-                       st, counts, s.nb, row_order);
+  const size_t slab = (size_t)rows * w.words;
+  hipLaunchKernelGGL(union_rows_kernel, dim3((rows + kMaskThreads - 1) / kMaskThreads),
+                     dim3(kMaskThreads), 0, st, masks, n_masks, slab, rows, s.nb, w.words, flags,
+                     counts, umask);
+  launch_csr(s, counts, umask, row_ptr, col_idx, row_order, st);
+  return hipGetLastError();
+}
+
+// out[x] = OR over i of masks[i * slab + x]; out may be one of the masks.
+__global__ void __launch_bounds__(kMaskThreads)
+mask_union_kernel(const uint64_t* masks, int n_masks, size_t slab, uint64_t* out) {
+  for (size_t x = (size_t)blockIdx.x * kMaskThreads + threadIdx.x; x < slab;
+       x += (size_t)gridDim.x * kMaskThreads) {
+    uint64_t m = 0;
+    for (int i = 0; i < n_masks; ++i) m |= masks[(size_t)i * slab + x];
+    out[x] = m;
+  }
+}
+
+hipError_t launch_mask_union(const Dims& s, const uint64_t* masks, int n_masks, uint64_t* out,
+                             hipStream_t st) {
+  const size_t slab = (size_t)s.bh * s.nb * mask_words(s);
+  const size_t blocks = (slab + kMaskThreads - 1) / kMaskThreads;
+  hipLaunchKernelGGL(mask_union_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)),
+                     dim3(kMaskThreads), 0, st, masks, n_masks, slab, out);
+  return hipGetLastError();
+}
+
+// Sum over a 1024-thread block; the result is valid in thread 0.
+template <typename T>
+__device__ __forceinline__ T block_sum_1024(T x, T* wsum) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+  if (lane == 0) wsum[wave] = x;
+  __syncthreads();
+  T t = 0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < 16; ++i) t += wsum[i];
+  return t;
+}
+
+// counts[0] = |A & B|, counts[1] = |A | B| (set bits), one work-group.
+__global__ void __launch_bounds__(1024)
+mask_overlap_kernel(const uint64_t* __restrict__ a, const uint64_t* __restrict__ b, size_t slab,
+                    int64_t* __restrict__ counts) {
+  __shared__ long long wsum[16];
+  long long inter = 0, uni = 0;
+  for (size_t x = threadIdx.x; x < slab; x += 1024) {
+    const uint64_t p = a[x], q = b[x];
+    inter += __builtin_popcountll(p & q);
+    uni += __builtin_popcountll(p | q);
+  }
+  const long long ti = block_sum_1024(inter, wsum);
+  __syncthreads();
+  const long long tu = block_sum_1024(uni, wsum);
+  if (threadIdx.x == 0) {
+    counts[0] = ti;
+    counts[1] = tu;
+  }
+}
+
+hipError_t launch_mask_overlap(const Dims& s, const uint64_t* a, const uint64_t* b,
+                               int64_t* counts, hipStream_t st) {
+  const size_t slab = (size_t)s.bh * s.nb * mask_words(s);
+  hipLaunchKernelGGL(mask_overlap_kernel, dim3(1), dim3(1024), 0, st, a, b, slab, counts);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Retained attention mass of a support
+// ---------------------------------------------------------------------------
+
+// One wave per row: row_mass[row] = (sum of r over the row's CSR blocks
+// kb <= qb, sum of r over kb <= qb), in fp64, lane-strided then a fixed
+// butterfly, so the result is bitwise reproducible.
+__global__ void __launch_bounds__(kSelWaves * 64)
+row_mass_kernel(const float* __restrict__ r, const int32_t* __restrict__ row_ptr,
+                const int32_t* __restrict__ col_idx, int rows, int nb,
+                double* __restrict__ row_mass) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kSelWaves + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int qb = row % nb;
+  const float* v = r + (size_t)row * nb;
+  double inside = 0.0, total = 0.0;
+  for (int kb = lane; kb <= qb; kb += 64) total += (double)v[kb];
+  for (int e = row_ptr[row] + lane; e < row_ptr[row + 1]; e += 64) {
+    const int kb = col_idx[e];
+    if (kb >= 0 && kb <= qb) inside += (double)v[kb];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    inside += __shfl_xor(inside, off, 64);
+    total += __shfl_xor(total, off, 64);
+  }
+  if (lane == 0) {
+    row_mass[2 * (size_t)row] = inside;
+    row_mass[2 * (size_t)row + 1] = total;
+  }
+}
+
+__global__ void __launch_bounds__(1024)
+mass_total_kernel(const double* __restrict__ row_mass, int rows, double* __restrict__ totals) {
+  __shared__ double wsum[16];
+  double inside = 0.0, total = 0.0;
+  for (int x = threadIdx.x; x < rows; x += 1024) {
+    inside += row_mass[2 * (size_t)x];
+    total += row_mass[2 * (size_t)x + 1];
+  }
+  const double ti = block_sum_1024(inside, wsum);
+  __syncthreads();
+  const double tt = block_sum_1024(total, wsum);
+  if (threadIdx.x == 0) {
+    totals[0] = ti;
+    totals[1] = tt;
+  }
+}
+
+hipError_t launch_support_mass(const Dims& s, const float* r, const int32_t* row_ptr,
+                               const int32_t* col_idx, double* row_mass, double* totals,
+                               hipStream_t st) {
+  const int rows = s.bh * s.nb;
+  hipLaunchKernelGGL(row_mass_kernel, dim3((rows + kSelWaves - 1) / kSelWaves),
+                     dim3(kSelWaves * 64), 0, st, r, row_ptr, col_idx, rows, s.nb, row_mass);
+  if (totals != nullptr)
+    hipLaunchKernelGGL(mass_total_kernel, dim3(1), dim3(1024), 0, st, row_mass, rows, totals);
   return hipGetLastError();
 }
 

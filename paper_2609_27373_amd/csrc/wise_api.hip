@@ -99,6 +99,79 @@ wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k, 
                                       (hipStream_t)hip_stream));
 }
 
+wise_status wise_select_step(const wise_shape* s, const float* r, float tau, uint64_t* mask,
+                             void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!r || !mask) return WISE_ERR_NULL;
+  if (d.nb > wise::kMaxSelectBlocks) return WISE_ERR_UNSUPPORTED;
+  if (!(tau > 0.f && tau <= 1.f)) return WISE_ERR_RANGE;
+  if (!aligned(r, 4) || !aligned(mask, 8)) return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_select_step(d, r, tau, mask, (hipStream_t)hip_stream));
+}
+
+wise_status wise_support_from_masks(const wise_shape* s, const uint64_t* masks, int32_t n_masks,
+                                    uint32_t flags, int32_t* row_ptr, int32_t* col_idx,
+                                    int32_t* row_order, void* workspace, size_t workspace_bytes,
+                                    void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!masks || !row_ptr || !col_idx || !workspace) return WISE_ERR_NULL;
+  if (d.nb > wise::kMaxSelectBlocks) return WISE_ERR_UNSUPPORTED;
+  if (n_masks < 1) return WISE_ERR_SHAPE;
+  if (flags & ~(uint32_t)(WISE_FORCE_SINK | WISE_FORCE_DIAG)) return WISE_ERR_RANGE;
+  if (workspace_bytes < wise::select_workspace_bytes(d)) return WISE_ERR_WORKSPACE;
+  if (!aligned(masks, 8) || !aligned(row_ptr, 4) || !aligned(col_idx, 4) ||
+      (row_order && !aligned(row_order, 4)) || !aligned(workspace, 256))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_support_from_masks(d, masks, n_masks, flags, row_ptr, col_idx,
+                                                  row_order, workspace,
+                                                  (hipStream_t)hip_stream));
+}
+
+wise_status wise_mask_union(const wise_shape* s, const uint64_t* masks, int32_t n_masks,
+                            uint64_t* out, void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!masks || !out) return WISE_ERR_NULL;
+  if (n_masks < 1) return WISE_ERR_SHAPE;
+  if (!aligned(masks, 8) || !aligned(out, 8)) return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_mask_union(d, masks, n_masks, out, (hipStream_t)hip_stream));
+}
+
+wise_status wise_mask_overlap(const wise_shape* s, const uint64_t* a, const uint64_t* b,
+                              int64_t* counts, void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!a || !b || !counts) return WISE_ERR_NULL;
+  if (!aligned(a, 8) || !aligned(b, 8) || !aligned(counts, 8)) return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_mask_overlap(d, a, b, counts, (hipStream_t)hip_stream));
+}
+
+wise_status wise_support_mass(const wise_shape* s, const float* r, const int32_t* row_ptr,
+                              const int32_t* col_idx, double* row_mass, double* totals,
+                              void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!r || !row_ptr || !col_idx || !row_mass) return WISE_ERR_NULL;
+  if (!aligned(r, 4) || !aligned(row_ptr, 4) || !aligned(col_idx, 4) || !aligned(row_mass, 8) ||
+      (totals && !aligned(totals, 8)))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_support_mass(d, r, row_ptr, col_idx, row_mass, totals,
+                                            (hipStream_t)hip_stream));
+}
+
+int32_t wise_mask_words(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return -1;
+  return wise::mask_words(d);
+}
+
 size_t wise_select_workspace_bytes(const wise_shape* s) {
   wise::Dims d;
   if (check_shape(s, &d) != WISE_OK) return 0;

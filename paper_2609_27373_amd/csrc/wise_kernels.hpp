@@ -27,5 +27,18 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
                          int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, void* ws,
                          hipStream_t st);
 size_t select_workspace_bytes(const Dims& s);
+int mask_words(const Dims& s);
+hipError_t launch_select_step(const Dims& s, const float* r, float tau, uint64_t* mask,
+                              hipStream_t st);
+hipError_t launch_support_from_masks(const Dims& s, const uint64_t* masks, int n_masks,
+                                     uint32_t flags, int32_t* row_ptr, int32_t* col_idx,
+                                     int32_t* row_order, void* ws, hipStream_t st);
+hipError_t launch_mask_union(const Dims& s, const uint64_t* masks, int n_masks, uint64_t* out,
+                             hipStream_t st);
+hipError_t launch_mask_overlap(const Dims& s, const uint64_t* a, const uint64_t* b,
+                               int64_t* counts, hipStream_t st);
+hipError_t launch_support_mass(const Dims& s, const float* r, const int32_t* row_ptr,
+                               const int32_t* col_idx, double* row_mass, double* totals,
+                               hipStream_t st);
 
 }  // namespace wise

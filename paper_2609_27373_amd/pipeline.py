@@ -2,10 +2,17 @@
 
 Section 5 of the paper in three phases, all on the device:
   discovery  steps 1..t_d: full causal attention; steps in the window also
-             pool their attention mass into the fp32 accumulator
+             pool their attention mass
   selection  once after step t_d: per-row support + CSR + row order
   reuse      steps t_d+1..T: attention restricted to the fixed support, with
              this step's Q/K/V
+
+Two selection rules (mode):
+  "accumulate"  the window steps' block masses are summed into one fp32
+                accumulator and selected once
+  "union"       the paper's eq. (block_working_set): each window step's
+                masses are selected on their own (B_q^(t, eta)) into a
+                bitmask, and the support is the union of those sets
 
 Buffers are allocated once per trajectory (torch device memory); every call
 enqueues on the current stream and returns.
@@ -19,15 +26,28 @@ from . import wise
 
 
 class WisePipeline:
+    MODES = ("accumulate", "union")
+
     def __init__(self, batch, heads, seq_len, head_dim, block, tau, flags=wise.WISE_DEFAULT_FLAGS,
-                 scale=0.0, device="cuda"):
+                 scale=0.0, device="cuda", mode="accumulate", window=4):
+        if mode not in self.MODES:
+            raise ValueError(f"mode must be one of {self.MODES}")
         self.shape = wise.make_shape(batch, heads, seq_len, head_dim, block, scale)
         self.tau = float(tau)
         self.flags = int(flags)
+        self.mode = mode
         nb = seq_len // block
+        # accumulate mode: the running sum; union mode: one step's masses
         self.acc = torch.zeros((batch, heads, nb, nb), dtype=torch.float32, device=device)
         self.lse = torch.empty((batch, heads, seq_len), dtype=torch.float32, device=device)
         self.schedule = wise.Schedule(self.shape, device)
+        self.window = int(window)
+        self.masks = None
+        if mode == "union":
+            words = wise.wise_mask_words(self.shape)
+            self.masks = torch.zeros((self.window, batch * heads * nb, words), dtype=torch.int64,
+                                     device=device)
+        self.filled = 0
 
     @classmethod
     def for_config(cls, cfg, tau=None, **kw):
@@ -36,10 +56,20 @@ class WisePipeline:
 
     def reset(self):
         self.acc.zero_()
+        self.filled = 0
 
     def discovery_step(self, q, k, v, out, accumulate: bool):
-        wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse,
-                                   self.acc if accumulate else None)
+        """One discovery step; `accumulate` marks a step of the window."""
+        if accumulate and self.mode == "union":
+            if self.filled >= self.window:
+                raise RuntimeError("more window steps than the union window holds")
+            self.acc.zero_()
+            wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse, self.acc)
+            wise.wise_select_step(self.shape, self.acc, self.tau, self.masks[self.filled])
+            self.filled += 1
+        else:
+            wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse,
+                                       self.acc if accumulate else None)
         return out
 
     def dense_step(self, q, k, v, out, lse=None):
@@ -47,7 +77,12 @@ class WisePipeline:
         return out
 
     def select(self):
-        self.schedule.select(self.acc, self.tau, self.flags)
+        if self.mode == "union":
+            if self.filled == 0:
+                raise RuntimeError("union mode: no window step was run before select()")
+            self.schedule.from_masks(self.masks, self.filled, self.flags)
+        else:
+            self.schedule.select(self.acc, self.tau, self.flags)
         return self.schedule
 
     def late_step(self, q, k, v, out, lse=None, ordered=True):

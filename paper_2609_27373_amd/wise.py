@@ -27,8 +27,9 @@ STATUS_NAMES = {0: "WISE_OK", 1: "WISE_ERR_NULL", 2: "WISE_ERR_SHAPE", 3: "WISE_
 
 # Every symbol include/wise.h declares.
 EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_sparse_attn",
-           "wise_select_workspace_bytes", "wise_support_capacity", "wise_status_string",
-           "wise_abi_version")
+           "wise_select_step", "wise_support_from_masks", "wise_mask_union", "wise_mask_overlap",
+           "wise_support_mass", "wise_mask_words", "wise_select_workspace_bytes",
+           "wise_support_capacity", "wise_status_string", "wise_abi_version")
 
 
 class WiseError(RuntimeError):
@@ -74,6 +75,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wise_select_support.restype = ctypes.c_int
     lib.wise_sparse_attn.argtypes = [S, P, P, P, P, P, P, P, P, P]
     lib.wise_sparse_attn.restype = ctypes.c_int
+    lib.wise_select_step.argtypes = [S, P, ctypes.c_float, P, P]
+    lib.wise_select_step.restype = ctypes.c_int
+    lib.wise_support_from_masks.argtypes = [S, P, ctypes.c_int32, ctypes.c_uint32, P, P, P, P,
+                                            ctypes.c_size_t, P]
+    lib.wise_support_from_masks.restype = ctypes.c_int
+    lib.wise_mask_union.argtypes = [S, P, ctypes.c_int32, P, P]
+    lib.wise_mask_union.restype = ctypes.c_int
+    lib.wise_mask_overlap.argtypes = [S, P, P, P, P]
+    lib.wise_mask_overlap.restype = ctypes.c_int
+    lib.wise_support_mass.argtypes = [S, P, P, P, P, P, P]
+    lib.wise_support_mass.restype = ctypes.c_int
+    lib.wise_mask_words.argtypes = [S]
+    lib.wise_mask_words.restype = ctypes.c_int32
     lib.wise_select_workspace_bytes.argtypes = [S]
     lib.wise_select_workspace_bytes.restype = ctypes.c_size_t
     lib.wise_support_capacity.argtypes = [S]
@@ -154,6 +168,58 @@ def wise_sparse_attn(s: wise_shape, q, k, v, row_ptr, col_idx, row_order, o, lse
         _ptr(lse, torch.float32, "lse", nlse), _stream(stream)), "wise_sparse_attn")
 
 
+def _mask_elems(s: wise_shape, n: int = 1) -> int:
+    return n * _sizes(s)[3] * max(wise_mask_words(s), 0)
+
+
+def wise_select_step(s: wise_shape, r, tau: float, mask, stream=None) -> None:
+    _, _, nacc, _ = _sizes(s)
+    _check(_lib().wise_select_step(
+        ctypes.byref(s), _ptr(r, torch.float32, "r", nacc), ctypes.c_float(tau),
+        _ptr(mask, torch.int64, "mask", _mask_elems(s)), _stream(stream)), "wise_select_step")
+
+
+def wise_support_from_masks(s: wise_shape, masks, n_masks: int, flags: int, row_ptr, col_idx,
+                            row_order=None, workspace=None, stream=None) -> None:
+    _, _, _, rows = _sizes(s)
+    i32 = torch.int32
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib().wise_support_from_masks(
+        ctypes.byref(s), _ptr(masks, torch.int64, "masks", _mask_elems(s, max(n_masks, 0))),
+        ctypes.c_int32(n_masks), ctypes.c_uint32(flags), _ptr(row_ptr, i32, "row_ptr", rows + 1),
+        _ptr(col_idx, i32, "col_idx"), _ptr(row_order, i32, "row_order", rows),
+        _ptr(workspace, None, "workspace"), ctypes.c_size_t(ws_bytes), _stream(stream)),
+        "wise_support_from_masks")
+
+
+def wise_mask_union(s: wise_shape, masks, n_masks: int, out, stream=None) -> None:
+    _check(_lib().wise_mask_union(
+        ctypes.byref(s), _ptr(masks, torch.int64, "masks", _mask_elems(s, max(n_masks, 0))),
+        ctypes.c_int32(n_masks), _ptr(out, torch.int64, "out", _mask_elems(s)), _stream(stream)),
+        "wise_mask_union")
+
+
+def wise_mask_overlap(s: wise_shape, a, b, counts, stream=None) -> None:
+    n = _mask_elems(s)
+    _check(_lib().wise_mask_overlap(
+        ctypes.byref(s), _ptr(a, torch.int64, "a", n), _ptr(b, torch.int64, "b", n),
+        _ptr(counts, torch.int64, "counts", 2), _stream(stream)), "wise_mask_overlap")
+
+
+def wise_support_mass(s: wise_shape, r, row_ptr, col_idx, row_mass, totals=None,
+                      stream=None) -> None:
+    _, _, nacc, rows = _sizes(s)
+    i32, f64 = torch.int32, torch.float64
+    _check(_lib().wise_support_mass(
+        ctypes.byref(s), _ptr(r, torch.float32, "r", nacc), _ptr(row_ptr, i32, "row_ptr", rows + 1),
+        _ptr(col_idx, i32, "col_idx"), _ptr(row_mass, f64, "row_mass", 2 * rows),
+        _ptr(totals, f64, "totals", 2), _stream(stream)), "wise_support_mass")
+
+
+def wise_mask_words(s: wise_shape) -> int:
+    return int(_lib().wise_mask_words(ctypes.byref(s)))
+
+
 def wise_select_workspace_bytes(s: wise_shape) -> int:
     return int(_lib().wise_select_workspace_bytes(ctypes.byref(s)))
 
@@ -189,6 +255,12 @@ class Schedule:
     def select(self, acc, tau: float, flags: int = WISE_DEFAULT_FLAGS, stream=None):
         wise_select_support(self.shape, acc, tau, flags, self.row_ptr, self.col_idx,
                             self.row_order, self.workspace, stream)
+        return self
+
+    def from_masks(self, masks, n_masks: int, flags: int = WISE_DEFAULT_FLAGS, stream=None):
+        """The union of n_masks per-step supports (back to back in `masks`)."""
+        wise_support_from_masks(self.shape, masks, n_masks, flags, self.row_ptr, self.col_idx,
+                                self.row_order, self.workspace, stream)
         return self
 
     def nnz(self) -> int:

@@ -43,7 +43,7 @@ def test_exports(lib):
 
 
 def test_version_and_strings(lib):
-    assert wise.wise_abi_version() == 1
+    assert wise.wise_abi_version() == 2
     for st, name in wise.STATUS_NAMES.items():
         assert wise.wise_status_string(st).startswith(name)
     assert "unknown" in wise.wise_status_string(99)
@@ -63,6 +63,10 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_support_capacity(s4) == 32 * 256 * 257 // 2
     assert wise.wise_support_capacity(S(seq_len=500)) == -1
     assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
+    assert wise.wise_mask_words(S()) == 1
+    assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
+    assert wise.wise_mask_words(s4) == 4
+    assert wise.wise_mask_words(S(seq_len=500)) == -1
 
 
 FAKE = ctypes.c_void_p(4096)        # aligned, never dereferenced: calls fail validation first
@@ -115,3 +119,50 @@ def test_select_validation(lib, case, status):
 def test_sparse_validation(lib, case, status):
     s = case.pop("s", S())
     assert sparse(lib, s, **case) == status
+
+
+MIS8 = ctypes.c_void_p(4096 + 4)    # 4-byte but not 8-byte aligned
+
+
+def sh(s):
+    return ctypes.byref(s) if s is not None else None
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(r=None), 1), (dict(mask=None), 1), (dict(tau=0.0), 4),
+    (dict(tau=1.01), 4), (dict(tau=float("nan")), 4), (dict(mask=MIS8), 2),
+    (dict(s=S(seq_len=64 * 2048)), 3), (dict(s=S(head_dim=80)), 3),
+])
+def test_select_step_validation(lib, case, status):
+    s = case.pop("s", S())
+    a = dict(r=FAKE, tau=0.9, mask=FAKE)
+    a.update(case)
+    assert lib.wise_select_step(sh(s), a["r"], ctypes.c_float(a["tau"]), a["mask"], None) == status
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(masks=None), 1), (dict(rp=None), 1), (dict(ws=None), 1),
+    (dict(n=0), 2), (dict(n=-3), 2), (dict(flags=8), 4), (dict(wsb=16), 5),
+    (dict(masks=MIS8), 2), (dict(s=S(seq_len=64 * 2048)), 3),
+])
+def test_support_from_masks_validation(lib, case, status):
+    s = case.pop("s", S())
+    a = dict(masks=FAKE, n=4, flags=3, rp=FAKE, ci=FAKE, ws=FAKE, wsb=1 << 30)
+    a.update(case)
+    assert lib.wise_support_from_masks(sh(s), a["masks"], a["n"], a["flags"], a["rp"], a["ci"],
+                                       None, a["ws"], a["wsb"], None) == status
+
+
+@pytest.mark.parametrize("fn,args,status", [
+    ("wise_mask_union", (None, 2, FAKE), 1), ("wise_mask_union", (FAKE, 0, FAKE), 2),
+    ("wise_mask_union", (FAKE, 2, MIS8), 2), ("wise_mask_union", (FAKE, 1, None), 1),
+    ("wise_mask_overlap", (FAKE, None, FAKE), 1), ("wise_mask_overlap", (FAKE, FAKE, MIS8), 2),
+    ("wise_support_mass", (FAKE, FAKE, FAKE, None, None), 1),
+    ("wise_support_mass", (None, FAKE, FAKE, FAKE, None), 1),
+    ("wise_support_mass", (FAKE, FAKE, FAKE, MIS8, None), 2),
+    ("wise_support_mass", (FAKE, FAKE, FAKE, FAKE, MIS8), 2),
+])
+def test_mask_and_mass_validation(lib, fn, args, status):
+    assert getattr(lib, fn)(sh(S()), *args, None) == status
+    assert getattr(lib, fn)(None, *args, None) == 1
+    assert getattr(lib, fn)(sh(S(head_dim=80)), *args, None) == 3

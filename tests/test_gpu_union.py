@@ -1,0 +1,292 @@
+"""GPU parity of the paper's temporal-union working set and of the routing
+diagnostics, through the C ABI, against the CPU oracle.
+
+  wise_select_step          per-step sets B_q^(t, eta): bit-exact against the
+                            oracle's selection on the same fp32 masses
+  wise_support_from_masks   union CSR + row order: bit-exact against the
+                            oracle's union of the same masses
+  wise_mask_union / overlap rolling sets and their (intersection, union)
+                            sizes: exact integers
+  wise_support_mass         per-row retained mass: fp64 sums of the same fp32
+                            values, agreeing to 1e-12 relative; the fraction
+                            also checked against the oracle's probabilities
+                            (to the block-mass tolerance)
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import wise_oracle as O
+from paper_2609_27373_amd import diagnostics
+from paper_2609_27373_amd.pipeline import WisePipeline
+from paper_2609_27373_amd.workloads import CONFIGS, Trajectory
+from parity_util import ACC_TOL, assert_attn, f64, near_tie, say
+
+pytestmark = pytest.mark.gpu
+
+
+def mask_rows(mask, nb):
+    """Device bitmask [rows][words] (int64) -> list over rows of block ids."""
+    m = mask.cpu().numpy().view(np.uint64).reshape(-1, mask.shape[-1])
+    bits = np.unpackbits(m.view(np.uint8).reshape(m.shape[0], -1), axis=1, bitorder="little")
+    return [list(np.nonzero(b[:nb])[0]) for b in bits]
+
+
+def rows_to_mask(rows, nb, words):
+    m = np.zeros((len(rows), words), dtype=np.uint64)
+    for i, r in enumerate(rows):
+        for kb in r:
+            m[i, kb >> 6] |= np.uint64(1) << np.uint64(kb & 63)
+    return torch.from_numpy(m.view(np.int64)).cuda()
+
+
+def random_masses(bt, h, nb, seed, steps=1, ties=False):
+    """Positive causal rows summing to 1 (fp32); `ties` repeats values so
+    the (mass desc, block asc) tie rule decides."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(steps):
+        r = rng.gamma(0.3, size=(bt, h, nb, nb))
+        if ties:
+            r = np.round(r * 4) / 4 + 1e-3
+        r = r * np.tril(np.ones((nb, nb)))
+        out.append((r / r.sum(-1, keepdims=True)).astype(np.float32))
+    return out
+
+
+def shape_of(w, bt, h, nb, B=64, d=64):
+    return w.make_shape(bt, h, nb * B, d, B)
+
+
+@pytest.mark.parametrize("nb,seed,ties", [(1, 0, False), (9, 1, True), (64, 2, False),
+                                          (65, 3, True), (130, 4, False), (300, 5, False)])
+def test_select_step_parity(gpu_lib, nb, seed, ties):
+    w = gpu_lib
+    say(f"select_step nb={nb} seed={seed} ties={ties}")
+    bt, h = 1, 2
+    (r,) = random_masses(bt, h, nb, seed, ties=ties)
+    s = shape_of(w, bt, h, nb)
+    words = w.wise_mask_words(s)
+    mask = torch.full((bt * h * nb, words), -1, dtype=torch.int64, device="cuda")  # stale bits
+    for tau in (0.5, 0.9, 0.95, 1.0):
+        t32 = float(np.float32(tau))
+        w.wise_select_step(s, torch.from_numpy(r).cuda(), t32, mask)
+        torch.cuda.synchronize()
+        assert mask_rows(mask, 64 * words) == O.step_supports(r, t32), f"tau {tau}"
+
+
+@pytest.mark.parametrize("nb,steps,seed", [(1, 1, 0), (12, 4, 1), (64, 4, 2), (100, 3, 3),
+                                           (257, 4, 4)])
+def test_union_csr_parity(gpu_lib, nb, steps, seed):
+    w = gpu_lib
+    say(f"union CSR nb={nb} steps={steps} seed={seed}")
+    bt, h = 2, 2
+    ms = random_masses(bt, h, nb, seed, steps=steps)
+    s = shape_of(w, bt, h, nb)
+    rows, words = bt * h * nb, w.wise_mask_words(s)
+    masks = torch.empty((steps, rows, words), dtype=torch.int64, device="cuda")
+    tau = float(np.float32(0.9))
+    for i, m in enumerate(ms):
+        w.wise_select_step(s, torch.from_numpy(m).cuda(), tau, masks[i])
+    sched = w.Schedule(s)
+    for flags in (0, w.WISE_FORCE_SINK, w.WISE_FORCE_DIAG, w.WISE_DEFAULT_FLAGS):
+        sched.from_masks(masks, steps, flags)
+        torch.cuda.synchronize()
+        rp = sched.row_ptr.cpu().numpy()
+        ci = sched.col_idx[: int(rp[-1])].cpu().numpy()
+        rp_o, ci_o = O.select_support_union(ms, tau, flags)
+        assert np.array_equal(rp, rp_o) and np.array_equal(ci, ci_o), f"flags {flags}"
+        assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp_o, nb))
+
+
+def test_union_ignores_bits_past_the_diagonal(gpu_lib):
+    w = gpu_lib
+    bt, h, nb = 1, 1, 70
+    s = shape_of(w, bt, h, nb)
+    words = w.wise_mask_words(s)
+    rng = np.random.default_rng(7)
+    rows = [sorted(set(rng.integers(0, 128, size=5).tolist())) for _ in range(nb)]
+    say("union with stray bits past the diagonal (and past nb)")
+    masks = rows_to_mask(rows, nb, words)
+    sched = w.Schedule(s)
+    sched.from_masks(masks, 1, 0)
+    torch.cuda.synchronize()
+    rp = sched.row_ptr.cpu().numpy()
+    got = [list(sched.col_idx[rp[i]:rp[i + 1]].cpu().numpy()) for i in range(nb)]
+    want = [[kb for kb in r if kb <= qb] or [qb] for qb, r in enumerate(rows)]
+    assert got == want
+
+
+@pytest.mark.parametrize("nb,seed", [(5, 0), (64, 1), (190, 2)])
+def test_mask_union_and_overlap(gpu_lib, nb, seed):
+    w = gpu_lib
+    say(f"mask union / overlap nb={nb}")
+    bt, h = 1, 3
+    s = shape_of(w, bt, h, nb)
+    rows, words = bt * h * nb, w.wise_mask_words(s)
+    rng = np.random.default_rng(seed)
+    per_step = [[sorted(set(rng.integers(0, qb + 1, size=3).tolist())) for qb in
+                 [i % nb for i in range(rows)]] for _ in range(6)]
+    slab = torch.stack([rows_to_mask(p, nb, words) for p in per_step])
+    out = torch.empty((rows, words), dtype=torch.int64, device="cuda")
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    prev = None
+    for t in range(1, 7):
+        lo = max(1, t - 3)
+        w.wise_mask_union(s, slab[lo - 1:t].contiguous(), t - lo + 1, out)
+        torch.cuda.synchronize()
+        want = O.rolling_working_set(per_step, t)
+        assert mask_rows(out, 64 * words) == want, f"W^({t})"
+        if prev is not None:
+            w.wise_mask_overlap(s, prev, out, counts)
+            torch.cuda.synchronize()
+            assert tuple(counts.cpu().tolist()) == O.overlap_counts(
+                O.rolling_working_set(per_step, t - 1), want)
+        prev = out.clone()
+    # in place: out coincides with the first mask
+    buf = slab[:3].clone()
+    w.wise_mask_union(s, buf, 3, buf[0])
+    torch.cuda.synchronize()
+    assert torch.equal(buf[0], slab[0] | slab[1] | slab[2])
+
+
+@pytest.mark.parametrize("nb,seed", [(1, 0), (33, 1), (128, 2), (260, 3)])
+def test_support_mass_parity(gpu_lib, nb, seed):
+    w = gpu_lib
+    say(f"support mass nb={nb}")
+    bt, h = 2, 2
+    (r,) = random_masses(bt, h, nb, seed)
+    s = shape_of(w, bt, h, nb)
+    rng = np.random.default_rng(seed)
+    rp, ci = [0], []
+    for _ in range(bt * h):
+        for qb in range(nb):
+            k = int(rng.integers(1, qb + 2))
+            ci.extend(sorted(rng.choice(qb + 1, size=k, replace=False).tolist()))
+            rp.append(len(ci))
+    rp, ci = np.array(rp, np.int32), np.array(ci, np.int32)
+    row_mass = torch.empty((bt * h * nb, 2), dtype=torch.float64, device="cuda")
+    totals = torch.empty(2, dtype=torch.float64, device="cuda")
+    w.wise_support_mass(s, torch.from_numpy(r).cuda(), torch.from_numpy(rp).cuda(),
+                        torch.from_numpy(ci).cuda(), row_mass, totals)
+    torch.cuda.synchronize()
+    want = O.support_block_mass(r, rp, ci)
+    got = row_mass.cpu().numpy()
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-15)
+    t = totals.cpu().numpy()
+    np.testing.assert_allclose(t, want.sum(0), rtol=1e-12)
+
+
+def test_retained_mass_against_probabilities(gpu_lib):
+    """The GPU's fraction (block masses of its own dense pass) against the
+    oracle's from the attention probabilities of the same bf16 inputs."""
+    w = gpu_lib
+    bt, h, n, d, B = 1, 2, 512, 64, 64
+    say(f"retained mass vs probabilities bt={bt} h={h} n={n} d={d} B={B}")
+    g = torch.Generator().manual_seed(11)
+    q, k, v = [(torch.randn((bt, h, n, d), generator=g) * sc).to(torch.bfloat16)
+               for sc in (2.0, 1.0, 1.0)]
+    s = w.make_shape(bt, h, n, d, B)
+    nb = n // B
+    rng = np.random.default_rng(3)
+    rp, ci = [0], []
+    for _ in range(bt * h):
+        for qb in range(nb):
+            ci.extend(sorted({0, qb} | set(rng.integers(0, qb + 1, size=2).tolist())))
+            rp.append(len(ci))
+    rp, ci = np.array(rp, np.int32), np.array(ci, np.int32)
+    sched = w.Schedule(s)
+    sched.row_ptr.copy_(torch.from_numpy(rp))
+    sched.col_idx[: ci.size].copy_(torch.from_numpy(ci))
+    frac, row_mass = diagnostics.retained_mass(s, q.cuda(), k.cuda(), v.cuda(), sched)
+    per_head, want = O.retained_mass(f64(q), f64(k), rp, ci, B)
+    say(f"  retained {frac:.6f} oracle {want:.6f}")
+    assert abs(frac - want) <= ACC_TOL
+    rm = row_mass.cpu().numpy()
+    np.testing.assert_allclose(rm[:, 1], 1.0, atol=ACC_TOL)
+
+
+def test_union_trajectory_tiny(gpu_lib):
+    """Union mode end to end on the tiny workload: per-step masses on the
+    GPU, union CSR bit-exact on those masses, end to end against the
+    oracle's own masses (near-ties reported), and late-step attention."""
+    cfg = CONFIGS["tiny"]
+    say(f"union trajectory {cfg.name}")
+    tr = Trajectory(cfg, device="cpu")
+    steps = [tr.next(torch.bfloat16) for _ in range(cfg.steps)]
+    pipe = WisePipeline.for_config(cfg, mode="union")
+    out = torch.empty(steps[0][0].shape, dtype=torch.bfloat16, device="cuda")
+    gpu_r = []
+    pipe.reset()
+    for t in range(1, cfg.discovery_steps + 1):
+        q, k, v = (x.cuda() for x in steps[t - 1])
+        pipe.discovery_step(q, k, v, out, accumulate=t in cfg.window)
+        if t in cfg.window:
+            gpu_r.append(pipe.acc.cpu().numpy().copy())
+    pipe.select()
+    torch.cuda.synchronize()
+    tau = float(np.float32(cfg.tau))
+    nb = cfg.nb
+    rp = pipe.schedule.row_ptr.cpu().numpy()
+    ci = pipe.schedule.col_idx[: int(rp[-1])].cpu().numpy()
+    rp_o, ci_o = O.select_support_union(gpu_r, tau, pipe.flags)
+    assert np.array_equal(rp, rp_o) and np.array_equal(ci, ci_o)
+    # end to end: the oracle's masses from the same inputs
+    ref_r = [O.block_mass(f64(steps[t - 1][0]), f64(steps[t - 1][1]), cfg.block)
+             for t in cfg.window]
+    for a, b in zip(gpu_r, ref_r):
+        assert np.abs(a - b).max() <= ACC_TOL
+    rows_o = O.csr_rows(*O.select_support_union(ref_r, tau, pipe.flags))
+    rows_g = O.csr_rows(rp, ci)
+    for i, (g_, o_) in enumerate(zip(rows_g, rows_o)):
+        if g_ != o_:
+            assert any(near_tie(r.reshape(-1, nb)[i], i % nb, tau) for r in ref_r), i
+            say(f"  near-tie row {i} reported")
+    q, k, v = steps[cfg.discovery_steps]
+    pipe.late_step(q.cuda(), k.cuda(), v.cuda(), out)
+    torch.cuda.synchronize()
+    o_ref, _ = O.sparse_attention(f64(q), f64(k), f64(v), rp, ci, cfg.block)
+    assert_attn(out, o_ref, "union late step")
+
+
+@pytest.mark.parametrize("name", ["4k-pr", "8k"])
+def test_union_fullsize(gpu_lib, name):
+    """Full-size union mode: CSR bit-exact on the GPU's own per-step masses
+    for every row, sampled rows of the masses against the oracle, the union
+    contains the accumulate-mode support's per-step sets, and the retained
+    mass / rolling stability diagnostics run at that size."""
+    cfg = CONFIGS[name]
+    say(f"union full-size {name}")
+    tr = Trajectory(cfg, device="cuda")
+    pipe = WisePipeline.for_config(cfg, mode="union")
+    tau = float(np.float32(cfg.tau))
+    out = None
+    gpu_r, kept = [], {}
+    nb, B = cfg.nb, cfg.block
+    for t in range(1, cfg.discovery_steps + 2):
+        q, k, v = tr.next(torch.bfloat16)
+        if out is None:
+            out = torch.empty_like(q)
+        if t <= cfg.discovery_steps:
+            pipe.discovery_step(q, k, v, out, accumulate=t in cfg.window)
+            if t in cfg.window:
+                gpu_r.append(pipe.acc.cpu().numpy().copy())
+                kept[t] = (q[0, 0].float().cpu().double().numpy(),
+                           k[0, 0].float().cpu().double().numpy())
+        else:
+            pipe.select()
+            frac, _ = diagnostics.retained_mass(pipe.shape, q, k, v, pipe.schedule)
+    torch.cuda.synchronize()
+    rp = pipe.schedule.row_ptr.cpu().numpy()
+    ci = pipe.schedule.col_idx[: int(rp[-1])].cpu().numpy()
+    rp_o, ci_o = O.select_support_union(gpu_r, tau, pipe.flags)
+    assert np.array_equal(rp, rp_o) and np.array_equal(ci, ci_o)
+    for j, t in enumerate(cfg.window):
+        qh, kh = kept[t]
+        for qb in (0, nb // 2, nb - 1):
+            ref = O.block_mass_row(qh, kh, qb, B, 1.0 / np.sqrt(cfg.head_dim))
+            assert np.abs(gpu_r[j][0, 0, qb] - ref).max() <= ACC_TOL
+    dens = rp[-1] / (cfg.batch * cfg.heads * nb * (nb + 1) / 2)
+    say(f"  union density {dens:.4f}, retained future mass (step t_d+1) {frac:.4f}")
+    assert 0.0 < frac <= 1.0 + 1e-9 and frac >= 0.9 * cfg.tau
