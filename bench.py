@@ -44,7 +44,7 @@ PEAK_HBM_GBS = 8000.0
 # the same counter reads for one plain 256 MiB device copy (fetch x2, write
 # x1).  They hold only for the kernel source they were taken on: any other
 # digest of the sources reports null.
-MEASURED_TRAFFIC = {"4k": {"digest": "a52ef1f5cb06fc67", "bytes": 195396147}}
+MEASURED_TRAFFIC = {"4k": {"digest": "7c327a2a96540eca", "bytes": 195396147}}
 KERNEL_SOURCES = ("attention.hip", "wise_device.hpp")
 
 
@@ -244,6 +244,8 @@ def main():
     ap.add_argument("--config", default="4k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-regime", action="store_true")
+    ap.add_argument("--no-paper-geometry", action="store_true",
+                    help="skip the 4K, 220-head, d 96, 32-key-block workload")
     ap.add_argument("--no-diagnostics", action="store_true",
                     help="skip the retained-mass / rolling-stability diagnostics")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -276,6 +278,12 @@ def main():
         pu = measure(CONFIGS["4k-pr"], args.steps, args.warmup, mode="union",
                      diag=not args.no_diagnostics)
         log(f"[bench] paper-regime, union of per-step supports {json.dumps(pu)}")
+    pg = {}
+    if not args.no_paper_geometry and args.config == "4k":
+        for mode in ("union", "accumulate"):
+            pg[mode] = measure(CONFIGS["4k-b32"], args.steps, args.warmup, mode=mode,
+                               diag=not args.no_diagnostics)
+            log(f"[bench] paper geometry ({mode}) {json.dumps(pg[mode])}")
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -316,6 +324,8 @@ def main():
             k: (round(v, 5) if isinstance(v, float) else v) for k, v in pr.items()},
         "paper_regime_union": None if pu is None else {
             k: (round(v, 5) if isinstance(v, float) else v) for k, v in pu.items()},
+        "paper_geometry": {m: {k: (round(v, 5) if isinstance(v, float) else v) for k, v in r.items()}
+                           for m, r in pg.items()} or None,
         "context": "paper: up to 1.76x late-step speedup over FlashAttention at 4K on an RTX A6000",
     }
     print(json.dumps(line), flush=True)

@@ -29,8 +29,9 @@
  *    synchronisation.  WISE_ERR_HIP carries a failed launch.
  *  - Calls are stateless and re-entrant; calls on different streams with
  *    disjoint outputs may run concurrently.  No C++ exception crosses the ABI.
- *  - Supported: head_dim in {64, 96, 128}; block in {64, 128};
- *    seq_len % block == 0; nb <= 1024 for wise_select_support,
+ *  - Supported: head_dim in {64, 96, 128}; block in {32, 64, 128};
+ *    seq_len % block == 0, and seq_len % 64 == 0 for block 32 (the dense
+ *    kernel's key tiles); nb <= 1024 for wise_select_support,
  *    wise_select_step and wise_support_from_masks.
  *  - Support bitmasks (the union mode and the diagnostics): uint64
  *    [rows][words], words = wise_mask_words(s) = ceil(nb / 64); bit
@@ -56,8 +57,9 @@ extern "C" {
 typedef enum {
   WISE_OK = 0,
   WISE_ERR_NULL = 1,        /* a required pointer is NULL                    */
-  WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0,
-                               or a size that overflows int32 indexing       */
+  WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0
+                               (% 64 for block 32), a size that overflows
+                               int32 indexing, or a misaligned pointer       */
   WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
   WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, non-finite scale,
                                or unknown flag bit                           */

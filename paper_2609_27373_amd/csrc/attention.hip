@@ -27,17 +27,19 @@
 namespace wise {
 
 // ---------------------------------------------------------------------------
-// Global -> register -> LDS staging of one 64-key tile (K rows permuted so the
-// S^T accumulator comes out in PV operand order; V rows in natural order).
-// Loads for the next tile are issued before the current one is computed, so
-// the memory latency hides behind the MFMA work; stores follow the barrier
-// that retires the current tile.
+// Global -> register -> LDS staging of one tile of KT keys (64, or 32 for
+// 32-key blocks; K rows permuted so the S^T accumulator comes out in PV
+// operand order; V rows in natural order).  Loads for the next tile are
+// issued before the current one is computed, so the memory latency hides
+// behind the MFMA work; stores follow the barrier that retires the current
+// tile.
 // ---------------------------------------------------------------------------
-template <int D, int NT, bool kWithV>
+template <int D, int NT, bool kWithV, int KT = kKeyTile>
 struct TileStage {
   using G = Geo<D>;
+  static_assert(KT == 32 || KT == 64, "key tile");
   static constexpr int kRowChunks = D / 8;                    // 16-B chunks per key row
-  static constexpr int kChunks = kKeyTile * kRowChunks;       // per tensor
+  static constexpr int kChunks = KT * kRowChunks;             // per tensor
   static constexpr int kPer = (kChunks + NT - 1) / NT;
 
   u32x4_t kr[kPer];
@@ -105,35 +107,38 @@ struct WaveRows {
     l = 0.f;
   }
 
-  // S^T of one 64-key LDS tile: s[0] covers LDS rows 0..31, s[1] rows 32..63.
-  __device__ __forceinline__ void scores(const uint16_t* ks, int lane, f32x16_t s[2]) const {
+  // S^T of one LDS tile of 32*H keys: s[t] covers LDS rows 32t..32t+31.
+  template <int H>
+  __device__ __forceinline__ void scores(const uint16_t* ks, int lane, f32x16_t s[H]) const {
     const uint16_t* a0 = ks + (lane & 31) * G::kKStride + 8 * (lane >> 5);
     const uint16_t* a1 = a0 + 32 * G::kKStride;
     f32x16_t s0{}, s1{};
 #pragma unroll
     for (int c = 0; c < G::kDChunks; ++c) {
       s0 = mfma32x32x16(*(const u32x4_t*)(a0 + 16 * c), qf[c], s0);
-      s1 = mfma32x32x16(*(const u32x4_t*)(a1 + 16 * c), qf[c], s1);
+      if constexpr (H == 2) s1 = mfma32x32x16(*(const u32x4_t*)(a1 + 16 * c), qf[c], s1);
     }
     s[0] = s0;
-    s[1] = s1;
+    if constexpr (H == 2) s[1] = s1;
   }
 
   // Causal mask inside a tile: key0 + local key > query -> -inf.
-  __device__ __forceinline__ static void mask(f32x16_t s[2], int key0, int qi, int lane) {
+  template <int H>
+  __device__ __forceinline__ static void mask(f32x16_t s[H], int key0, int qi, int lane) {
     const int h = lane >> 5;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < H; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         if (key0 + score_key(t, r, h) > qi) s[t][r] = -INFINITY;
   }
 
   // Online softmax of one tile and O^T += V^T P^T.
-  __device__ __forceinline__ void softmax_pv(f32x16_t s[2], const uint16_t* vt, int lane, float c) {
+  template <int H>
+  __device__ __forceinline__ void softmax_pv(f32x16_t s[H], const uint16_t* vt, int lane, float c) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < H; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
     mx = pair_max(mx) * c;
@@ -152,13 +157,13 @@ struct WaveRows {
       m = mn;
     }
     const float mb = (m == -INFINITY) ? 0.f : m;
-    u32x4_t pb[4];
+    u32x4_t pb[2 * H];
     // The tile's probabilities are summed on their own and added to the row
     // sum once per tile: a long row (16K keys per lane at 32K) then carries
     // rounding error ~ tiles * eps instead of ~ keys * eps.
     float ts = 0.f;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < H; ++t) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[t][r], c, -mb));
@@ -177,7 +182,7 @@ struct WaveRows {
     const uint16_t* a = vt + (8 * (lane >> 5) + ((lane >> 2) & 3)) * G::kVStride +
                         16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+    for (int ks = 0; ks < 2 * H; ++ks)
 #pragma unroll
       for (int t = 0; t < G::kDTiles; ++t) {
         const u32x2_t lo = lds_read_tr16(a + (16 * ks) * G::kVStride + 32 * t);
@@ -189,15 +194,15 @@ struct WaveRows {
   // One tile: S^T, the causal mask when the tile reaches past this wave's
   // first query (only ever on diagonal tiles, and only instantiated for
   // them), online softmax and PV.
-  template <bool kMask>
+  template <bool kMask, int H = 2>
   __device__ __forceinline__ void attend(const uint16_t* ks, const uint16_t* vt, int lane,
                                          float c, int key0, int q0) {
-    f32x16_t s[2];
-    scores(ks, lane, s);
+    f32x16_t s[H];
+    scores<H>(ks, lane, s);
     if constexpr (kMask) {
-      if (key0 + kKeyTile - 1 > q0) mask(s, key0, q0 + (lane & 31), lane);
+      if (key0 + 32 * H - 1 > q0) mask<H>(s, key0, q0 + (lane & 31), lane);
     }
-    softmax_pv(s, vt, lane, c);
+    softmax_pv<H>(s, vt, lane, c);
   }
 
   // O = O^T / l written as bf16 rows; lse in natural log.
@@ -270,12 +275,14 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
 
 // ---------------------------------------------------------------------------
 // Block-sparse attention over a CSR support.  One work-group per (batch,
-// head, query block) row, NW = block/32 waves.  Schedule slot s (a logical id,
-// contiguous per XCD) runs row order[s]; wise_select_support writes the rows
-// of each head together, longest support first, so an XCD works through a
-// few heads at a time and their K/V tiles stay in its L2.
+// head, query block) row, NW = block/32 waves; key tiles of KT = min(block,
+// 64) keys, so a 32-key block is one 32-key tile and a one-wave group.
+// Schedule slot s (a logical id, contiguous per XCD) runs row order[s];
+// wise_select_support writes the rows of each head together, longest support
+// first, so an XCD works through a few heads at a time and their K/V tiles
+// stay in its L2.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
+template <int D, int NW, int KT>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
@@ -283,9 +290,10 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
                    uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
                    int group, float c) {
   using G = Geo<D>;
-  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
-  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
-  __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
+  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / KT, kH = KT / 32;
+  static_assert(kTPB >= 1 && kB % KT == 0, "block / key tile");
+  __shared__ __attribute__((aligned(16))) uint16_t ks[KT * G::kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[KT * G::kVStride];
   int sh, sit;
   sched_slot(gridDim.x / nb, nb, group, sh, sit);
   const int row = order ? order[sh * nb + sit] : sh * nb + (nb - 1 - sit);
@@ -304,13 +312,13 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   auto tile_key = [&](int it, bool& ok) {
     const int kb = col_idx[beg + it / kTPB];
     ok = (unsigned)kb <= (unsigned)qb;
-    return ok ? kb * kB + (it % kTPB) * kKeyTile : 0;
+    return ok ? kb * kB + (it % kTPB) * KT : 0;
   };
 
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
   w.reset();
-  TileStage<D, kNT, true> st;
+  TileStage<D, kNT, true, KT> st;
   const int ntiles = nent * kTPB;
   // Entries are ascending, so only the last one can be the diagonal block:
   // every earlier tile lies wholly below this group's queries.
@@ -324,7 +332,7 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     bool ok_next;
     const int key_next = tile_key(it + 1, ok_next);
     st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
-    if (ok && key0 + kKeyTile - 1 < qb * kB) w.template attend<false>(ks, vt, lane, c, key0, q0);
+    if (ok && key0 + KT - 1 < qb * kB) w.template attend<false, kH>(ks, vt, lane, c, key0, q0);
     __syncthreads();
     key0 = key_next;
     ok = ok_next;
@@ -335,7 +343,7 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     bool ok_next = false;
     const int key_next = (it + 1 < ntiles) ? tile_key(it + 1, ok_next) : 0;
     if (it + 1 < ntiles) st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
-    if (ok && key0 <= q0) w.template attend<true>(ks, vt, lane, c, key0, q0);
+    if (ok && key0 <= q0) w.template attend<true, kH>(ks, vt, lane, c, key0, q0);
     __syncthreads();
     key0 = key_next;
     ok = ok_next;
@@ -383,14 +391,15 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
   const int rows = s.bh * s.nb;
-  if (s.block == 64)
-    hipLaunchKernelGGL((sparse_attn_kernel<D, 2>), dim3(rows), dim3(128), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh),
-                       c);
+  if (s.block == 32)
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 1, 32>), dim3(rows), dim3(64), 0, st, Q, K, V, rp,
+                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
+  else if (s.block == 64)
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 2, 64>), dim3(rows), dim3(128), 0, st, Q, K, V, rp,
+                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
   else
-    hipLaunchKernelGGL((sparse_attn_kernel<D, 4>), dim3(rows), dim3(256), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh),
-                       c);
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 4, 64>), dim3(rows), dim3(256), 0, st, Q, K, V, rp,
+                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
   return hipGetLastError();
 }
 

@@ -6,7 +6,8 @@
 // pass.
 //
 // One work-group per (batch, head, query block), NW = block/32 waves, each
-// wave 32 queries.  S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K from
+// wave 32 queries.  With 32-key blocks a 64-key tile spans two key blocks,
+// and the wave pools each half of its scores into its own block.  S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K from
 // LDS, B = Q^T in registers), so every lane holds 32 scores of one query.
 // K tiles of 64 keys are staged global -> registers -> LDS, the loads of
 // the next tile issued before the current one is computed.  The group owns
@@ -72,7 +73,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)
 block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const float* __restrict__ lse, float* __restrict__ acc, int n, int nb,
                   int group, float c) {
-  constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / kKeyTile;
+  constexpr int kNT = NW * 64, kB = NW * 32;
   constexpr int kStride = kMassKStride(D);
   __shared__ __attribute__((aligned(16))) uint16_t ks[kKeyTile * kStride];
   __shared__ float red[NW];
@@ -94,9 +95,45 @@ block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   }
   const float nl = -lse[(size_t)bh * n + qi] * kLog2e;   // -log2 of the row normaliser
   const uint16_t* Kh = K + hoff;
-  const int ntiles = (qb + 1) * kTPB;
   KStage<D, kNT> st;
   st.load(Kh, tid);
+  if constexpr (kB == 32) {
+    // Tile it holds key blocks 2it (s[0]) and 2it+1 (s[1]); keys past the
+    // query are masked, which also drops a block 2it+1 > qb whole.
+    const int ntiles = (qb + 2) / 2;
+    for (int it = 0; it < ntiles; ++it) {
+      st.store(ks, tid);
+      __syncthreads();
+      if (it + 1 < ntiles) st.load(Kh + (size_t)(it + 1) * kKeyTile * D, tid);
+      const int key0 = it * kKeyTile;
+      const uint16_t* a0 = ks + (lane & 31) * kStride + 8 * (lane >> 5);
+      const uint16_t* a1 = a0 + 32 * kStride;
+      f32x16_t s[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+      for (int k = 0; k < D / 16; ++k) {
+        s[0] = mfma32x32x16(*(const u32x4_t*)(a0 + 16 * k), qf[k], s[0]);
+        s[1] = mfma32x32x16(*(const u32x4_t*)(a1 + 16 * k), qf[k], s[1]);
+      }
+      const bool diag = key0 + kKeyTile - 1 > q0;
+      float part[2] = {0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool keep = !diag || key0 + mass_key(t, r, lane >> 5) <= qi;
+          part[t] += keep ? fast_exp2(__builtin_fmaf(s[t][r], c, nl)) : 0.f;
+        }
+      const float b0 = wave_sum(part[0]), b1 = wave_sum(part[1]);
+      if (lane == 0) {
+        arow[2 * it] += b0 * (1.f / kB);
+        if (2 * it + 1 <= qb) arow[2 * it + 1] += b1 * (1.f / kB);
+      }
+      __syncthreads();
+    }
+    return;
+  }
+  constexpr int kTPB = kB / kKeyTile;
+  const int ntiles = (qb + 1) * kTPB;
   float blk = 0.f;
   for (int it = 0; it < ntiles; ++it) {
     st.store(ks, tid);
@@ -144,7 +181,10 @@ static hipError_t launch_mass_d(const Dims& s, const void* q, const void* k, con
   const float c = s.scale * kLog2e;
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
-  if (s.block == 64)
+  if (s.block == 32)
+    hipLaunchKernelGGL((block_mass_kernel<D, 1>), dim3(s.bh * s.nb), dim3(64), 0, st, Q, K, lse,
+                       acc, s.n, s.nb, sched_group(s.bh), c);
+  else if (s.block == 64)
     hipLaunchKernelGGL((block_mass_kernel<D, 2>), dim3(s.bh * s.nb), dim3(128), 0, st, Q, K, lse,
                        acc, s.n, s.nb, sched_group(s.bh), c);
   else

@@ -63,6 +63,7 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_support_capacity(s4) == 32 * 256 * 257 // 2
     assert wise.wise_support_capacity(S(seq_len=500)) == -1
     assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
+    assert wise.wise_support_capacity(S(block=32)) == 2 * 16 * 17 // 2
     assert wise.wise_mask_words(S()) == 1
     assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
     assert wise.wise_mask_words(s4) == 4
@@ -91,7 +92,8 @@ def sparse(lib, s, q=FAKE, rp=FAKE, ci=FAKE, o=FAKE):
 @pytest.mark.parametrize("case,status", [
     (dict(s=None), 1), (dict(q=None), 1), (dict(o=None), 1), (dict(acc=FAKE), 1),
     (dict(s=S(seq_len=500)), 2), (dict(s=S(batch=0)), 2), (dict(s=S(heads=-1)), 2),
-    (dict(s=S(head_dim=80)), 3), (dict(s=S(block=32)), 3), (dict(q=MIS), 2),
+    (dict(s=S(head_dim=80)), 3), (dict(s=S(block=16)), 3), (dict(q=MIS), 2),
+    (dict(s=S(block=32, seq_len=96)), 2), (dict(s=S(block=256)), 3),
     (dict(s=S(scale=float("inf"))), 4), (dict(s=S(scale=float("nan"))), 4),
     (dict(s=S(batch=4096, heads=4096, seq_len=1024, block=64)), 2),
 ])

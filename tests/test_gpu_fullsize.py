@@ -24,7 +24,7 @@ def sample_rows(cfg, k=4):
     return sorted(picks)[:k]
 
 
-@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k"])
+@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k", "4k-b32"])
 def test_fullsize_trajectory(gpu_lib, name):
     cfg = CONFIGS[name]
     say(f"full-size {name}: B={cfg.batch} H={cfg.heads} n={cfg.seq_len} d={cfg.head_dim} "
