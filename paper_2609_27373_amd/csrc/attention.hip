@@ -232,14 +232,14 @@ template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-                  float* __restrict__ lse, int n, int qtiles, int group, float c) {
+                  float* __restrict__ lse, int n, Sched sc, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kQT = NW * 32;
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
   __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
   int bh, item;
-  sched_slot(gridDim.x / qtiles, qtiles, group, bh, item);
-  const int qt = qtiles - 1 - item;
+  if (!sched_slot(sc, bh, item)) return;
+  const int qt = sc.items - 1 - item;
   const size_t hoff = (size_t)bh * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
@@ -288,14 +288,14 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
                    const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
                    uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
-                   int group, float c) {
+                   Sched sc, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / KT, kH = KT / 32;
   static_assert(kTPB >= 1 && kB % KT == 0, "block / key tile");
   __shared__ __attribute__((aligned(16))) uint16_t ks[KT * G::kKStride];
   __shared__ __attribute__((aligned(16))) uint16_t vt[KT * G::kVStride];
   int sh, sit;
-  sched_slot(gridDim.x / nb, nb, group, sh, sit);
+  if (!sched_slot(sc, sh, sit)) return;
   const int row = order ? order[sh * nb + sit] : sh * nb + (nb - 1 - sit);
   if ((unsigned)row >= (unsigned)rows) return;
   const int bh = row / nb, qb = row % nb;
@@ -361,14 +361,15 @@ static hipError_t launch_dense_d(const Dims& s, const void* q, const void* k, co
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
+  const size_t kv = (size_t)s.n * D * 4;
   if (s.n % 128 == 0) {
-    const int qt = s.n / 128;
-    hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(s.bh * qt), dim3(256), 0, st, Q, K, V,
-                       (uint16_t*)o, lse, s.n, qt, sched_group(s.bh), c);
+    const Sched sc = make_sched(s.bh, s.n / 128, kv);
+    hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(sched_grid(sc)), dim3(256), 0, st, Q, K,
+                       V, (uint16_t*)o, lse, s.n, sc, c);
   } else {
-    const int qt = s.n / 64;
-    hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(s.bh * qt), dim3(128), 0, st, Q, K, V,
-                       (uint16_t*)o, lse, s.n, qt, sched_group(s.bh), c);
+    const Sched sc = make_sched(s.bh, s.n / 64, kv);
+    hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(sched_grid(sc)), dim3(128), 0, st, Q, K,
+                       V, (uint16_t*)o, lse, s.n, sc, c);
   }
   return hipGetLastError();
 }
@@ -391,15 +392,17 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
   const int rows = s.bh * s.nb;
+  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 4);
+  const dim3 grid(sched_grid(sc));
   if (s.block == 32)
-    hipLaunchKernelGGL((sparse_attn_kernel<D, 1, 32>), dim3(rows), dim3(64), 0, st, Q, K, V, rp,
-                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 1, 32>), grid, dim3(64), 0, st, Q, K, V, rp, ci,
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
   else if (s.block == 64)
-    hipLaunchKernelGGL((sparse_attn_kernel<D, 2, 64>), dim3(rows), dim3(128), 0, st, Q, K, V, rp,
-                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 2, 64>), grid, dim3(128), 0, st, Q, K, V, rp, ci,
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
   else
-    hipLaunchKernelGGL((sparse_attn_kernel<D, 4, 64>), dim3(rows), dim3(256), 0, st, Q, K, V, rp,
-                       ci, order, (uint16_t*)o, lse, s.n, s.nb, rows, sched_group(s.bh), c);
+    hipLaunchKernelGGL((sparse_attn_kernel<D, 4, 64>), grid, dim3(256), 0, st, Q, K, V, rp, ci,
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
   return hipGetLastError();
 }
 

@@ -72,13 +72,13 @@ template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const float* __restrict__ lse, float* __restrict__ acc, int n, int nb,
-                  int group, float c) {
+                  Sched sc, float c) {
   constexpr int kNT = NW * 64, kB = NW * 32;
   constexpr int kStride = kMassKStride(D);
   __shared__ __attribute__((aligned(16))) uint16_t ks[kKeyTile * kStride];
   __shared__ float red[NW];
   int bh, item;
-  sched_slot(gridDim.x / nb, nb, group, bh, item);
+  if (!sched_slot(sc, bh, item)) return;
   const int qb = nb - 1 - item;   // the last (longest) query blocks first
   const size_t hoff = (size_t)bh * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -181,15 +181,17 @@ static hipError_t launch_mass_d(const Dims& s, const void* q, const void* k, con
   const float c = s.scale * kLog2e;
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
+  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 2);
+  const dim3 grid(sched_grid(sc));
   if (s.block == 32)
-    hipLaunchKernelGGL((block_mass_kernel<D, 1>), dim3(s.bh * s.nb), dim3(64), 0, st, Q, K, lse,
-                       acc, s.n, s.nb, sched_group(s.bh), c);
+    hipLaunchKernelGGL((block_mass_kernel<D, 1>), grid, dim3(64), 0, st, Q, K, lse, acc, s.n,
+                       s.nb, sc, c);
   else if (s.block == 64)
-    hipLaunchKernelGGL((block_mass_kernel<D, 2>), dim3(s.bh * s.nb), dim3(128), 0, st, Q, K, lse,
-                       acc, s.n, s.nb, sched_group(s.bh), c);
+    hipLaunchKernelGGL((block_mass_kernel<D, 2>), grid, dim3(128), 0, st, Q, K, lse, acc, s.n,
+                       s.nb, sc, c);
   else
-    hipLaunchKernelGGL((block_mass_kernel<D, 4>), dim3(s.bh * s.nb), dim3(256), 0, st, Q, K, lse,
-                       acc, s.n, s.nb, sched_group(s.bh), c);
+    hipLaunchKernelGGL((block_mass_kernel<D, 4>), grid, dim3(256), 0, st, Q, K, lse, acc, s.n,
+                       s.nb, sc, c);
   return hipGetLastError();
 }
 

@@ -98,33 +98,67 @@ __device__ __forceinline__ int k_lds_row(int key) {
   return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
-// Schedule slot of this work-group in a grid of heads * items work-groups:
-// `item` counts from the heaviest piece of a head (0) to the lightest.  The
-// hardware deals work-groups round-robin over the 8 XCDs in id order, so an
-// XCD receives every 8th id.  When heads % 8 == 0 each XCD owns a contiguous
-// range of heads (their K/V stay in its L2) and walks them in groups of
-// `group` heads, item-major inside a group: the heaviest items of the group's
-// heads start together, so no long item is left for the tail (head-major
-// order would leave them there), while only `group` heads compete for the
-// L2 at a time.  Otherwise the whole grid is item-major.
-__device__ __forceinline__ void sched_slot(int heads, int items, int group, int& head, int& item) {
-  const int b = blockIdx.x;
-  if (heads % 8 == 0) {
-    const int hp = heads / 8, j = b >> 3;
-    const int g = j / (group * items), gh = min(group, hp - g * group);
-    const int r = j - g * group * items;
-    head = (b & 7) * hp + g * group + r % gh;
-    item = r / gh;
-  } else {
-    head = b % heads;
-    item = b / heads;
+// Work order of the attention and block-mass grids.  A grid covers
+// heads * items pieces of work, `item` counting from the heaviest piece of a
+// head (0) to the lightest.  The hardware deals work-groups round-robin over
+// the 8 XCDs in id order, so an XCD receives every 8th id.  When the heads
+// split evenly enough over 8 XCDs (at least 8 heads, the busiest XCD within
+// 10% of an even share), each XCD owns a contiguous range of heads, so a
+// head's K/V stays in one L2; an XCD with one head fewer than per_xcd, and a
+// short last group, leave empty slots that return at once.  An XCD walks its
+// heads in groups of `group` heads, item-major inside a group: the heaviest
+// items of the group's heads start together, so no long item is left for the
+// tail (head-major order would leave them there), while only `group` heads
+// compete for the L2 at a time.  Otherwise the whole grid is item-major.
+struct Sched {
+  int heads, items, group, per_xcd;   // per_xcd == 0: whole grid item-major
+};
+
+// Host: the schedule for `heads` x `items` pieces whose heads each stream
+// kv_bytes of K/V.  Group size: every head of the XCD when 8 divides the
+// head count (measured at 4K / 32 heads / block 64: interleaving 2 heads at a
+// time keeps more K/V in L2, 112 instead of 154 MiB fetched per sparse
+// launch, but balances worse and runs 5% slower; that grid runs in about two
+// rounds of resident work-groups per XCD).  Otherwise as many heads as fit
+// about 3 MiB of the 4 MiB L2 (many heads per XCD, many rounds of work).
+inline Sched make_sched(int heads, int items, size_t kv_bytes) {
+  Sched s{heads, items, 1, 0};
+  const int per = (heads + 7) / 8;
+  // The busiest XCD holds `per` heads against an even share of heads / 8:
+  // partition only while that costs at most 10%.
+  if (heads >= 8 && 80 * per <= 11 * heads) {
+    s.per_xcd = per;
+    if (heads % 8 == 0) {
+      s.group = s.per_xcd;
+    } else {
+      const size_t fit = kv_bytes > 0 ? (size_t)(3u << 20) / kv_bytes : 1;
+      s.group = (int)(fit < 1 ? 1 : (fit > (size_t)s.per_xcd ? (size_t)s.per_xcd : fit));
+    }
   }
+  return s;
 }
 
-// Heads interleaved per XCD: all of its heads.  (Measured at 4K with 32
-// heads: interleaving fewer heads at a time keeps more K/V in the L2 - 112
-// instead of 154 MiB fetched per sparse launch - but balances worse and runs
-// 5% slower; the HBM traffic stays far below the bandwidth either way.)
-inline int sched_group(int heads) { return heads % 8 == 0 ? heads / 8 : 1; }
+inline unsigned sched_grid(const Sched& s) {
+  return (unsigned)(s.per_xcd ? 8 * s.per_xcd * s.items : s.heads * s.items);
+}
+
+// Device: (head, item) of this work-group; false for an empty slot.
+__device__ __forceinline__ bool sched_slot(const Sched& s, int& head, int& item) {
+  const int b = blockIdx.x;
+  if (s.per_xcd == 0) {
+    head = b % s.heads;
+    item = b / s.heads;
+    return true;
+  }
+  const int x = b & 7, j = b >> 3;
+  const int lo = (x * s.heads) >> 3, cnt = (((x + 1) * s.heads) >> 3) - lo;
+  const int g = j / (s.group * s.items);
+  if (g * s.group >= cnt) return false;
+  const int gh = min(s.group, cnt - g * s.group);
+  const int r = j - g * s.group * s.items;
+  head = lo + g * s.group + r % gh;
+  item = r / gh;
+  return item < s.items;   // a short last group leaves empty slots
+}
 
 }  // namespace wise
