@@ -27,6 +27,12 @@ fusion or reordering beyond what the definition states:
                           a step that falls inside a support, from the
                           attention probabilities themselves
   support_block_mass      the same quantity from block masses, per row
+  expand_kv               grouped-query attention (Appendix B: the second
+                          backbone has 32 query heads sharing 8 key-value
+                          heads): query head h reads key-value head
+                          h // (heads / kv_heads); expanding K, V to one copy
+                          per query head turns every function above into its
+                          grouped form
   schedule_order          per-head longest-support-first ordering of CSR rows
   sparse_attention        Section 5.2, eq. (wise_attention), gather form
   sparse_attention_masked Section 5.2, eq. (wise_attention) with the mask R
@@ -52,6 +58,21 @@ def _f64(x):
 def default_scale(d: int) -> float:
     """1/sqrt(d_h), the temperature of Section 3, eq. (recurrent_attention)."""
     return 1.0 / np.sqrt(float(d))
+
+
+def kv_head(h, heads, kv_heads):
+    """Key-value head read by query head h under grouped-query attention."""
+    if heads % kv_heads:
+        raise ValueError("heads must be a multiple of kv_heads")
+    return h // (heads // kv_heads)
+
+
+def expand_kv(x, heads):
+    """[bt][kv_heads][n][d] -> [bt][heads][n][d]: query head h gets a copy
+    of key-value head kv_head(h, heads, kv_heads)."""
+    x = _f64(x)
+    kvh = x.shape[1]
+    return x[:, [kv_head(h, heads, kvh) for h in range(heads)]]
 
 
 # ---------------------------------------------------------------------------

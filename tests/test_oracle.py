@@ -346,6 +346,27 @@ def test_retained_mass_two_routes_agree(seed):
     np.testing.assert_allclose(hp, per_head, atol=1e-12)
 
 
+def test_gqa_expand_against_brute_force():
+    """Grouped-query attention: 4 query heads over 2 key-value heads, each
+    head checked against the scalar loops on its own key-value head."""
+    q = rnd((1, 4, 9, 3), 21)
+    kv = rnd((2, 1, 2, 9, 3), 22)
+    k, v = kv[0], kv[1]
+    assert [O.kv_head(h, 4, 2) for h in range(4)] == [0, 0, 1, 1]
+    assert [O.kv_head(h, 6, 3) for h in range(6)] == [0, 0, 1, 1, 2, 2]
+    o, lse = O.dense_attention(q, O.expand_kv(k, 4), O.expand_kv(v, 4))
+    for h in range(4):
+        g = h // 2
+        _, Ob, Lb = brute.attention(q[0, h].tolist(), k[0, g].tolist(), v[0, g].tolist(),
+                                    1 / math.sqrt(3))
+        np.testing.assert_allclose(o[0, h], np.array(Ob), atol=1e-12)
+        np.testing.assert_allclose(lse[0, h], np.array(Lb), atol=1e-12)
+    # one group per head is plain multi-head attention
+    np.testing.assert_array_equal(O.expand_kv(rnd((2, 3, 4, 2), 5), 3), rnd((2, 3, 4, 2), 5))
+    with pytest.raises(ValueError):
+        O.kv_head(0, 6, 4)
+
+
 def test_margins_example():
     m = O.support_margins(np.array([0.1, 0.6, 0.3]), 2, 0.8)
     assert m["kstar"] == 2
