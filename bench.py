@@ -284,6 +284,9 @@ def main():
             pg[mode] = measure(CONFIGS["4k-b32"], args.steps, args.warmup, mode=mode,
                                diag=not args.no_diagnostics)
             log(f"[bench] paper geometry ({mode}) {json.dumps(pg[mode])}")
+        pg["grouped_query_union"] = measure(CONFIGS["4k-gqa"], args.steps, args.warmup,
+                                            mode="union", diag=not args.no_diagnostics)
+        log(f"[bench] grouped-query geometry (union) {json.dumps(pg['grouped_query_union'])}")
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

@@ -18,9 +18,12 @@
  *    contiguous, row-major.  The library allocates nothing.
  *  - bf16 tensors are raw IEEE bfloat16 storage (uint16, round-to-nearest-even
  *    when produced by the library).
- *  - Shapes: q, k, v, o are [batch][heads][seq_len][head_dim];
- *    lse is [batch][heads][seq_len]; acc is [batch][heads][nb][nb] with
- *    nb = seq_len / block.  CSR row r = (b * heads + h) * nb + qb.
+ *  - Shapes: q, o are [batch][heads][seq_len][head_dim]; k, v are
+ *    [batch][kv_heads][seq_len][head_dim] (kv_heads = heads without
+ *    grouped-query attention); lse is [batch][heads][seq_len]; acc is
+ *    [batch][heads][nb][nb] with nb = seq_len / block.  CSR row
+ *    r = (b * heads + h) * nb + qb: masses, supports and rows stay per query
+ *    head, and query head h reads key-value head h / (heads / kv_heads).
  *  - Every call validates its arguments on the host BEFORE touching the
  *    device and returns a status; on any error nothing is launched and no
  *    output is written.  On success the work is only enqueued on
@@ -58,8 +61,9 @@ typedef enum {
   WISE_OK = 0,
   WISE_ERR_NULL = 1,        /* a required pointer is NULL                    */
   WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0
-                               (% 64 for block 32), a size that overflows
-                               int32 indexing, or a misaligned pointer       */
+                               (% 64 for block 32), heads % kv_heads != 0,
+                               a size that overflows int32 indexing, or a
+                               misaligned pointer                            */
   WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
   WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, non-finite scale,
                                or unknown flag bit                           */
@@ -69,7 +73,10 @@ typedef enum {
 
 /* Problem geometry shared by all calls.  scale <= 0 selects 1/sqrt(head_dim),
  * the softmax temperature of the paper's attention (Section 3, eq.
- * "recurrent_attention"). */
+ * "recurrent_attention").  kv_heads: key-value heads for grouped-query
+ * attention (the paper's second backbone shares 8 key-value heads among 32
+ * query heads, Appendix B); 0 means kv_heads = heads; heads must be a
+ * multiple of it. */
 typedef struct {
   int32_t batch;
   int32_t heads;
@@ -77,6 +84,7 @@ typedef struct {
   int32_t head_dim;
   int32_t block;
   float scale;
+  int32_t kv_heads;
 } wise_shape;
 
 /* Selection flags: blocks forced into every support after the cumulative-mass
@@ -98,8 +106,9 @@ enum {
  *     acc[b][h][qb][kb] += (1/block) * sum_{i in I_qb} sum_{j in I_kb, j<=i} A_ij
  *       (Section 5.1, eq. "block_attention_mass"); entries kb > qb untouched.
  *
- *   q, k, v : bf16 [batch][heads][seq_len][head_dim], read-only.
- *   o       : bf16, same shape, written.
+ *   q       : bf16 [batch][heads][seq_len][head_dim], read-only.
+ *   k, v    : bf16 [batch][kv_heads][seq_len][head_dim], read-only.
+ *   o       : bf16, same shape as q, written.
  *   lse     : fp32 [batch][heads][seq_len] or NULL.  Must be non-NULL when
  *             acc != NULL (the pooled probabilities use it).
  *   acc     : fp32 [batch][heads][nb][nb] or NULL (plain dense attention).
@@ -155,7 +164,8 @@ wise_status wise_select_support(const wise_shape* s, const float* acc,
  *   O = softmax(Q K^T * scale + M + R) V,  R_ij = 0 if kb(j) in S_{qb(i)},
  *   -inf otherwise.  Q/K/V are this step's; only the support is reused.
  *
- *   q, k, v   : bf16 [batch][heads][seq_len][head_dim], read-only.
+ *   q         : bf16 [batch][heads][seq_len][head_dim], read-only.
+ *   k, v      : bf16 [batch][kv_heads][seq_len][head_dim], read-only.
  *   row_ptr   : int32 [rows + 1], col_idx : int32 [nnz] — a CSR whose rows
  *               list key-block ids in strictly ascending order with every id
  *               <= qb (as written by wise_select_support).  Ids outside

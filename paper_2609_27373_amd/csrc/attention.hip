@@ -232,7 +232,7 @@ template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-                  float* __restrict__ lse, int n, Sched sc, float c) {
+                  float* __restrict__ lse, int n, int heads, int gq, Sched sc, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kQT = NW * 32;
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
@@ -241,6 +241,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   if (!sched_slot(sc, bh, item)) return;
   const int qt = sc.items - 1 - item;
   const size_t hoff = (size_t)bh * n * D;
+  const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
 
@@ -249,8 +250,8 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   w.reset();
   // Tiles 0 .. nfull-1 lie wholly below every query of the group; the last
   // kQT/64 tiles hold the diagonal and are masked per wave.
-  const uint16_t* Kh = K + hoff;
-  const uint16_t* Vh = V + hoff;
+  const uint16_t* Kh = K + kvoff;
+  const uint16_t* Vh = V + kvoff;
   const int ntiles = (qbase + kQT) / kKeyTile;
   const int nfull = qbase / kKeyTile;
   TileStage<D, kNT, true> st;
@@ -288,7 +289,7 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
                    const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
                    uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
-                   Sched sc, float c) {
+                   int heads, int gq, Sched sc, float c) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kB = NW * 32, kTPB = kB / KT, kH = KT / 32;
   static_assert(kTPB >= 1 && kB % KT == 0, "block / key tile");
@@ -304,8 +305,9 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int q0 = qb * kB + 32 * wave;
   const int beg = row_ptr[row];
   const int nent = row_ptr[row + 1] - beg;
-  const uint16_t* Kh = K + hoff;
-  const uint16_t* Vh = V + hoff;
+  const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
+  const uint16_t* Kh = K + kvoff;
+  const uint16_t* Vh = V + kvoff;
 
   // Tile it of the row: entry it / kTPB, sub-tile it % kTPB.  Ids outside
   // 0..qb are skipped (their tile is never loaded out of bounds nor used).
@@ -361,15 +363,15 @@ static hipError_t launch_dense_d(const Dims& s, const void* q, const void* k, co
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
-  const size_t kv = (size_t)s.n * D * 4;
+  const size_t kv = (size_t)s.n * D * 4 / s.gq;   // K/V bytes per query head
   if (s.n % 128 == 0) {
     const Sched sc = make_sched(s.bh, s.n / 128, kv);
     hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(sched_grid(sc)), dim3(256), 0, st, Q, K,
-                       V, (uint16_t*)o, lse, s.n, sc, c);
+                       V, (uint16_t*)o, lse, s.n, s.heads, s.gq, sc, c);
   } else {
     const Sched sc = make_sched(s.bh, s.n / 64, kv);
     hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(sched_grid(sc)), dim3(128), 0, st, Q, K,
-                       V, (uint16_t*)o, lse, s.n, sc, c);
+                       V, (uint16_t*)o, lse, s.n, s.heads, s.gq, sc, c);
   }
   return hipGetLastError();
 }
@@ -392,17 +394,17 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
   const int rows = s.bh * s.nb;
-  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 4);
+  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 4 / s.gq);
   const dim3 grid(sched_grid(sc));
   if (s.block == 32)
     hipLaunchKernelGGL((sparse_attn_kernel<D, 1, 32>), grid, dim3(64), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
   else if (s.block == 64)
     hipLaunchKernelGGL((sparse_attn_kernel<D, 2, 64>), grid, dim3(128), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
   else
     hipLaunchKernelGGL((sparse_attn_kernel<D, 4, 64>), grid, dim3(256), 0, st, Q, K, V, rp, ci,
-                       order, (uint16_t*)o, lse, s.n, s.nb, rows, sc, c);
+                       order, (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
   return hipGetLastError();
 }
 

@@ -72,7 +72,7 @@ template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const float* __restrict__ lse, float* __restrict__ acc, int n, int nb,
-                  Sched sc, float c) {
+                  int heads, int gq, Sched sc, float c) {
   constexpr int kNT = NW * 64, kB = NW * 32;
   constexpr int kStride = kMassKStride(D);
   __shared__ __attribute__((aligned(16))) uint16_t ks[kKeyTile * kStride];
@@ -94,7 +94,7 @@ block_mass_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
     for (int k = 0; k < D / 16; ++k) qf[k] = *(const u32x4_t*)(row + 16 * k);
   }
   const float nl = -lse[(size_t)bh * n + qi] * kLog2e;   // -log2 of the row normaliser
-  const uint16_t* Kh = K + hoff;
+  const uint16_t* Kh = K + (size_t)kv_head(bh, heads, gq) * n * D;
   KStage<D, kNT> st;
   st.load(Kh, tid);
   if constexpr (kB == 32) {
@@ -181,17 +181,17 @@ static hipError_t launch_mass_d(const Dims& s, const void* q, const void* k, con
   const float c = s.scale * kLog2e;
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
-  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 2);
+  const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 2 / s.gq);
   const dim3 grid(sched_grid(sc));
   if (s.block == 32)
     hipLaunchKernelGGL((block_mass_kernel<D, 1>), grid, dim3(64), 0, st, Q, K, lse, acc, s.n,
-                       s.nb, sc, c);
+                       s.nb, s.heads, s.gq, sc, c);
   else if (s.block == 64)
     hipLaunchKernelGGL((block_mass_kernel<D, 2>), grid, dim3(128), 0, st, Q, K, lse, acc, s.n,
-                       s.nb, sc, c);
+                       s.nb, s.heads, s.gq, sc, c);
   else
     hipLaunchKernelGGL((block_mass_kernel<D, 4>), grid, dim3(256), 0, st, Q, K, lse, acc, s.n,
-                       s.nb, sc, c);
+                       s.nb, s.heads, s.gq, sc, c);
   return hipGetLastError();
 }
 

@@ -25,6 +25,8 @@ wise_status check_shape(const wise_shape* s, wise::Dims* out) {
   if (s->block != 32 && s->block != 64 && s->block != 128) return WISE_ERR_UNSUPPORTED;
   if (s->seq_len % s->block != 0) return WISE_ERR_SHAPE;
   if (s->block == 32 && s->seq_len % 64 != 0) return WISE_ERR_SHAPE;   // 64-key dense tiles
+  const int32_t kvh = s->kv_heads == 0 ? s->heads : s->kv_heads;
+  if (kvh <= 0 || s->heads % kvh != 0) return WISE_ERR_SHAPE;
   if (isnan(s->scale) || isinf(s->scale)) return WISE_ERR_RANGE;
   const int64_t bh = (int64_t)s->batch * s->heads;
   const int64_t nb = s->seq_len / s->block;
@@ -35,6 +37,8 @@ wise_status check_shape(const wise_shape* s, wise::Dims* out) {
   out->d = s->head_dim;
   out->block = s->block;
   out->nb = (int)nb;
+  out->heads = s->heads;
+  out->gq = s->heads / kvh;
   out->scale = s->scale > 0.f ? s->scale : 1.0f / sqrtf((float)s->head_dim);
   return WISE_OK;
 }
@@ -191,7 +195,8 @@ const char* wise_status_string(wise_status st) {
     case WISE_ERR_NULL: return "WISE_ERR_NULL: a required pointer is NULL";
     case WISE_ERR_SHAPE:
       return "WISE_ERR_SHAPE: invalid geometry, seq_len not a multiple of block (of 64 for block "
-             "32), size beyond int32 CSR indexing, or a misaligned pointer";
+             "32), heads not a multiple of kv_heads, size beyond int32 CSR indexing, or a "
+             "misaligned pointer";
     case WISE_ERR_UNSUPPORTED:
       return "WISE_ERR_UNSUPPORTED: head_dim must be 64/96/128, block 32/64/128, seq_len/block "
              "<= 1024 for selection";

@@ -98,6 +98,12 @@ __device__ __forceinline__ int k_lds_row(int key) {
   return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
+// Key-value head of flattened query head bh = b * heads + h when gq query
+// heads share one key-value head: b * (heads / gq) + h / gq.
+__device__ __forceinline__ int kv_head(int bh, int heads, int gq) {
+  return gq == 1 ? bh : (bh / heads) * (heads / gq) + (bh % heads) / gq;
+}
+
 // Work order of the attention and block-mass grids.  A grid covers
 // heads * items pieces of work, `item` counting from the heaviest piece of a
 // head (0) to the lightest.  The hardware deals work-groups round-robin over

@@ -8,9 +8,10 @@
 
 namespace wise {
 
-// Validated geometry: bh = batch * heads, nb = n / block.
+// Validated geometry: bh = batch * heads, nb = n / block; gq = heads /
+// kv_heads query heads share one key-value head.
 struct Dims {
-  int bh, n, d, block, nb;
+  int bh, n, d, block, nb, heads, gq;
   float scale;
 };
 

@@ -29,10 +29,10 @@ class WisePipeline:
     MODES = ("accumulate", "union")
 
     def __init__(self, batch, heads, seq_len, head_dim, block, tau, flags=wise.WISE_DEFAULT_FLAGS,
-                 scale=0.0, device="cuda", mode="accumulate", window=4):
+                 scale=0.0, device="cuda", mode="accumulate", window=4, kv_heads=0):
         if mode not in self.MODES:
             raise ValueError(f"mode must be one of {self.MODES}")
-        self.shape = wise.make_shape(batch, heads, seq_len, head_dim, block, scale)
+        self.shape = wise.make_shape(batch, heads, seq_len, head_dim, block, scale, kv_heads)
         self.tau = float(tau)
         self.flags = int(flags)
         self.mode = mode
@@ -52,7 +52,7 @@ class WisePipeline:
     @classmethod
     def for_config(cls, cfg, tau=None, **kw):
         return cls(cfg.batch, cfg.heads, cfg.seq_len, cfg.head_dim, cfg.block,
-                   cfg.tau if tau is None else tau, **kw)
+                   cfg.tau if tau is None else tau, kv_heads=cfg.kv_heads, **kw)
 
     def reset(self):
         self.acc.zero_()

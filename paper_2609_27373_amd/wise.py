@@ -42,16 +42,19 @@ class WiseError(RuntimeError):
 class wise_shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32),
                 ("seq_len", ctypes.c_int32), ("head_dim", ctypes.c_int32),
-                ("block", ctypes.c_int32), ("scale", ctypes.c_float)]
+                ("block", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("kv_heads", ctypes.c_int32)]
 
     def __repr__(self):
         return (f"wise_shape(batch={self.batch}, heads={self.heads}, seq_len={self.seq_len}, "
-                f"head_dim={self.head_dim}, block={self.block}, scale={self.scale})")
+                f"head_dim={self.head_dim}, block={self.block}, scale={self.scale}, "
+                f"kv_heads={self.kv_heads})")
 
 
 def make_shape(batch: int, heads: int, seq_len: int, head_dim: int, block: int,
-               scale: float = 0.0) -> wise_shape:
-    return wise_shape(batch, heads, seq_len, head_dim, block, scale)
+               scale: float = 0.0, kv_heads: int = 0) -> wise_shape:
+    """kv_heads = 0: one key-value head per query head."""
+    return wise_shape(batch, heads, seq_len, head_dim, block, scale, kv_heads)
 
 
 _LIB: Optional[ctypes.CDLL] = None
@@ -135,11 +138,16 @@ def _sizes(s: wise_shape):
     return bh * s.seq_len * s.head_dim, bh * s.seq_len, bh * nb * nb, bh * nb
 
 
+def _kv_numel(s: wise_shape) -> int:
+    return s.batch * (s.kv_heads or s.heads) * s.seq_len * s.head_dim
+
+
 def wise_dense_attn_accum(s: wise_shape, q, k, v, o, lse=None, acc=None, stream=None) -> None:
     nqkv, nlse, nacc, _ = _sizes(s)
+    nkv = _kv_numel(s)
     bf = torch.bfloat16
     _check(_lib().wise_dense_attn_accum(
-        ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nqkv), _ptr(v, bf, "v", nqkv),
+        ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nkv), _ptr(v, bf, "v", nkv),
         _ptr(o, bf, "o", nqkv), _ptr(lse, torch.float32, "lse", nlse),
         _ptr(acc, torch.float32, "acc", nacc), _stream(stream)), "wise_dense_attn_accum")
 
@@ -160,9 +168,10 @@ def wise_select_support(s: wise_shape, acc, tau: float, flags: int, row_ptr, col
 def wise_sparse_attn(s: wise_shape, q, k, v, row_ptr, col_idx, row_order, o, lse=None,
                      stream=None) -> None:
     nqkv, nlse, _, rows = _sizes(s)
+    nkv = _kv_numel(s)
     bf, i32 = torch.bfloat16, torch.int32
     _check(_lib().wise_sparse_attn(
-        ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nqkv), _ptr(v, bf, "v", nqkv),
+        ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nkv), _ptr(v, bf, "v", nkv),
         _ptr(row_ptr, i32, "row_ptr", rows + 1), _ptr(col_idx, i32, "col_idx"),
         _ptr(row_order, i32, "row_order", rows), _ptr(o, bf, "o", nqkv),
         _ptr(lse, torch.float32, "lse", nlse), _stream(stream)), "wise_sparse_attn")

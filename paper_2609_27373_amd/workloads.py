@@ -17,6 +17,11 @@ roughly put, as in the paper's late steps.
 Readings of the workload text (all std, not variance):
   K0, V0 ~ N(0, 1)[n, d];  Q tile q = g * mean_{r in rel(q)} K0[tile r]
   + 0.5 * N(0, 1)[B, d];  eps_t ~ 0.02 * N(0, 1).  rel(0) = {0}.
+
+With grouped-query attention (kv_heads < heads) each key-value head draws
+its own K0, V0, and every query head of its group plants its own relevant
+blocks on that shared K0, so the query heads of a group keep different
+supports.
 """
 
 from __future__ import annotations
@@ -48,10 +53,19 @@ class WorkloadConfig:
     step_noise: float = 0.02  # std of the per-step random walk
     seed: int = 0
     dtype: str = "bf16"
+    kv_heads: int = 0          # grouped-query attention: key-value heads (0: = heads)
 
     @property
     def nb(self) -> int:
         return self.seq_len // self.block
+
+    @property
+    def kvh(self) -> int:
+        return self.kv_heads or self.heads
+
+    @property
+    def grouped(self) -> bool:
+        return self.kvh != self.heads
 
     @property
     def tau(self) -> float:
@@ -100,6 +114,13 @@ CONFIGS["4k-pr"] = CONFIGS["4k"].with_(name="4k-pr", gain=4.5)
 # support density in the paper's 37-45 % band at 4K with B = 32.
 CONFIGS["4k-b32"] = WorkloadConfig("4k-b32", 1, 220, 96, 4096, 32, 12, 20, (0.95,), (6, 6),
                                    sink=True, zipf=1.2, gain=7.5, seed=5)
+# Grouped-query attention with the second backbone's geometry (Appendix B:
+# 6 recurrent blocks, 32 query heads sharing 8 key-value heads; head_dim 64
+# of its Llama-3.2 base), the blocks as the batch, and the same WISE
+# configuration (B 32, t_d 12, 20 late steps, tau 0.95).  Gain 11 puts the
+# density in the 37-45 % band (head_dim 64 dilutes the planted logit).
+CONFIGS["4k-gqa"] = WorkloadConfig("4k-gqa", 6, 32, 64, 4096, 32, 12, 20, (0.95,), (6, 6),
+                                   sink=True, zipf=1.2, gain=11.0, seed=6, kv_heads=8)
 
 
 def relevant_blocks(cfg: WorkloadConfig) -> list:
@@ -151,6 +172,10 @@ def planted_base(cfg: WorkloadConfig, device="cpu", heads: Optional[Sequence[int
     depend only on (seed, head id), so a subset reproduces the full tensor's
     slices exactly.
     """
+    if cfg.grouped:
+        if heads is not None:
+            raise ValueError("head subsets are not drawn for grouped-query workloads")
+        return _planted_grouped(cfg, device)
     n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
     rel = relevant_blocks(cfg)
     ids = list(range(cfg.batch * cfg.heads)) if heads is None else list(heads)
@@ -175,6 +200,34 @@ def planted_base(cfg: WorkloadConfig, device="cpu", heads: Optional[Sequence[int
     return Q.reshape(shape), K.reshape(shape), V.reshape(shape)
 
 
+_KV_TAG = 1 << 20   # stream ids of key-value heads, apart from query heads
+
+
+def _planted_grouped(cfg: WorkloadConfig, device):
+    n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
+    G = cfg.heads // cfg.kvh
+    rel = relevant_blocks(cfg)
+    K = torch.empty((cfg.batch * cfg.kvh, n, d), dtype=torch.float32, device=device)
+    V = torch.empty_like(K)
+    for kid in range(cfg.batch * cfg.kvh):
+        g = _gen(device, cfg.seed, _KV_TAG + kid)
+        K[kid] = torch.randn((n, d), generator=g, device=device)
+        V[kid] = torch.randn((n, d), generator=g, device=device)
+    Q = torch.empty((cfg.batch * cfg.heads, n, d), dtype=torch.float32, device=device)
+    for hid in range(cfg.batch * cfg.heads):
+        b, h = divmod(hid, cfg.heads)
+        kid = b * cfg.kvh + h // G
+        g = _gen(device, cfg.seed, 1 + hid)
+        W = torch.zeros((nb, nb), dtype=torch.float32)
+        for q, r in enumerate(rel[hid]):
+            W[q, torch.as_tensor(r)] = 1.0 / len(r)
+        mean_tiles = W.to(device) @ K[kid].reshape(nb, B * d)
+        noise = torch.randn((nb, B * d), generator=g, device=device)
+        Q[hid] = (cfg.gain * mean_tiles + cfg.noise * noise).reshape(n, d)
+    return (Q.reshape(cfg.batch, cfg.heads, n, d), K.reshape(cfg.batch, cfg.kvh, n, d),
+            V.reshape(cfg.batch, cfg.kvh, n, d))
+
+
 class Trajectory:
     """Per-step inputs of one recurrent trajectory.
 
@@ -196,6 +249,10 @@ class Trajectory:
     def next(self, dtype=None):
         self.t += 1
         n, d = self.cfg.seq_len, self.cfg.head_dim
+        if self.cfg.grouped:
+            self._step_grouped()
+            dt = dtype or (torch.float32 if self.cfg.dtype == "fp32" else torch.bfloat16)
+            return tuple(x.to(dt).contiguous() for x in self.state)
         for slot, hid in enumerate(self.ids):
             g = _gen(self.device, self.cfg.seed, (1 + hid) * 65536 + self.t)
             for x in self.state:
@@ -204,3 +261,15 @@ class Trajectory:
                                 alpha=self.cfg.step_noise)
         dt = dtype or (torch.float32 if self.cfg.dtype == "fp32" else torch.bfloat16)
         return tuple(x.to(dt).contiguous() for x in self.state)
+
+    def _step_grouped(self):
+        n, d, c = self.cfg.seq_len, self.cfg.head_dim, self.cfg
+        q, k, v = (x.view(-1, n, d) for x in self.state)
+        for hid in range(c.batch * c.heads):
+            g = _gen(self.device, c.seed, (1 + hid) * 65536 + self.t)
+            q[hid].add_(torch.randn((n, d), generator=g, device=self.device), alpha=c.step_noise)
+        for kid in range(c.batch * c.kvh):
+            g = _gen(self.device, c.seed, (_KV_TAG + kid) * 65536 + self.t)
+            for x in (k, v):
+                x[kid].add_(torch.randn((n, d), generator=g, device=self.device),
+                            alpha=c.step_noise)

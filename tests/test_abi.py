@@ -94,6 +94,7 @@ def sparse(lib, s, q=FAKE, rp=FAKE, ci=FAKE, o=FAKE):
     (dict(s=S(seq_len=500)), 2), (dict(s=S(batch=0)), 2), (dict(s=S(heads=-1)), 2),
     (dict(s=S(head_dim=80)), 3), (dict(s=S(block=16)), 3), (dict(q=MIS), 2),
     (dict(s=S(block=32, seq_len=96)), 2), (dict(s=S(block=256)), 3),
+    (dict(s=S(heads=4, kv_heads=3)), 2), (dict(s=S(kv_heads=-1)), 2), (dict(s=S(kv_heads=4)), 2),
     (dict(s=S(scale=float("inf"))), 4), (dict(s=S(scale=float("nan"))), 4),
     (dict(s=S(batch=4096, heads=4096, seq_len=1024, block=64)), 2),
 ])

@@ -24,7 +24,7 @@ def sample_rows(cfg, k=4):
     return sorted(picks)[:k]
 
 
-@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k", "4k-b32"])
+@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k", "4k-b32", "4k-gqa"])
 def test_fullsize_trajectory(gpu_lib, name):
     cfg = CONFIGS[name]
     say(f"full-size {name}: B={cfg.batch} H={cfg.heads} n={cfg.seq_len} d={cfg.head_dim} "
@@ -37,6 +37,11 @@ def test_fullsize_trajectory(gpu_lib, name):
     need = set(cfg.window) | {cfg.discovery_steps, cfg.discovery_steps + 1}
     nb, B, d = cfg.nb, cfg.block, cfg.head_dim
     scale = 1.0 / np.sqrt(d)
+
+    def kvi(bh):   # key-value head of flattened query head bh
+        b, h = divmod(bh, cfg.heads)
+        return b * cfg.kvh + O.kv_head(h, cfg.heads, cfg.kvh)
+
     out = None
     for t in range(1, cfg.discovery_steps + 2):
         q, k, v = tr.next(torch.bfloat16)
@@ -44,7 +49,8 @@ def test_fullsize_trajectory(gpu_lib, name):
             out = torch.empty_like(q)
         flat = [x.view(-1, cfg.seq_len, d) for x in (q, k, v)]
         if t in need:
-            keep[t] = {h: tuple(x[h].float().cpu() for x in flat) for h in heads}
+            keep[t] = {h: (flat[0][h].float().cpu(), flat[1][kvi(h)].float().cpu(),
+                           flat[2][kvi(h)].float().cpu()) for h in heads}
         if t <= cfg.discovery_steps:
             pipe.discovery_step(q, k, v, out, accumulate=t in cfg.window)
             if t == cfg.discovery_steps:

@@ -10,6 +10,7 @@ from paper_2609_27373_amd.workloads import CONFIGS, Trajectory, planted_base, re
 def test_configs_divide():
     for c in CONFIGS.values():
         assert c.seq_len % c.block == 0 and c.head_dim in (64, 96, 128) and c.block in (32, 64, 128)
+        assert c.heads % c.kvh == 0
         assert 1 <= len(c.window) <= 4 and c.window[-1] == c.discovery_steps
 
 
@@ -74,3 +75,30 @@ def test_flop_accounting():
             want += sum(1 for b in s for j in range(b * B, (b + 1) * B) if j <= i)
     assert metrics.support_pairs(rp, ci, nb, B) == want
     assert abs(metrics.density(rp, nb, 1) - len(ci) / 10) < 1e-12
+
+
+def test_grouped_query_workload():
+    """Key-value heads are shared: every query head of a group is planted on
+    its group's K0, with its own relevant blocks; the walk moves K/V once per
+    key-value head."""
+    c = CONFIGS["tiny"].with_(batch=2, heads=4, kv_heads=2, seq_len=256)
+    q0, k0, v0 = planted_base(c)
+    assert q0.shape == (2, 4, 256, 64) and k0.shape == (2, 2, 256, 64) == v0.shape
+    rel = relevant_blocks(c)
+    B, nb = c.block, c.nb
+    for b in range(2):
+        for h in range(4):
+            kt = k0[b, h // 2].reshape(nb, B, -1)
+            for q in range(1, nb):
+                # the query tile minus its planted mean is the 0.5-std noise
+                resid = q0[b, h, q * B:(q + 1) * B] - c.gain * kt[rel[b * 4 + h][q]].mean(0)
+                assert abs(resid.std().item() - c.noise) < 0.05
+    tr, tr2 = Trajectory(c), Trajectory(c)
+    for _ in range(2):
+        a, a2 = tr.next(), tr2.next()
+    for x, y in zip(a, a2):
+        assert torch.equal(x, y)
+    assert a[1].shape == (2, 2, 256, 64)
+    import pytest
+    with pytest.raises(ValueError):
+        planted_base(c, heads=[0])
