@@ -129,7 +129,7 @@ def diagnose(cfg, pipe, steps):
     region): retained future full-attention mass of the frozen support on
     every late step, and the rolling working-set stability."""
     scratch = (torch.empty_like(steps[0][0]), torch.empty_like(pipe.lse),
-               torch.empty_like(pipe.acc))
+               torch.empty_like(pipe.acc), pipe.mass_ws)
     fr = [diagnostics.retained_mass(pipe.shape, *steps[t - 1], pipe.schedule, scratch)[0]
           for t in range(cfg.discovery_steps + 1, cfg.steps + 1)]
     st = diagnostics.rolling_stability(pipe.shape, steps, pipe.tau, cfg.discovery_steps)

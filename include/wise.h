@@ -15,7 +15,9 @@
  * Conventions shared by every call
  * --------------------------------
  *  - Every tensor argument is a DEVICE pointer owned by the caller,
- *    contiguous, row-major.  The library allocates nothing.
+ *    contiguous, row-major.  The library allocates nothing: scratch space
+ *    comes in as caller-owned workspaces sized by the *_workspace_bytes
+ *    queries.
  *  - bf16 tensors are raw IEEE bfloat16 storage (uint16, round-to-nearest-even
  *    when produced by the library).
  *  - Shapes: q, o are [batch][heads][seq_len][head_dim]; k, v are
@@ -67,7 +69,7 @@ typedef enum {
   WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
   WISE_ERR_RANGE = 4,       /* tau outside (0, 1] / NaN, non-finite scale,
                                or unknown flag bit                           */
-  WISE_ERR_WORKSPACE = 5,   /* workspace smaller than wise_select_workspace_bytes */
+  WISE_ERR_WORKSPACE = 5,   /* workspace smaller than the size query returns */
   WISE_ERR_HIP = 6          /* a HIP launch reported an error                */
 } wise_status;
 
@@ -109,18 +111,24 @@ enum {
  *   q       : bf16 [batch][heads][seq_len][head_dim], read-only.
  *   k, v    : bf16 [batch][kv_heads][seq_len][head_dim], read-only.
  *   o       : bf16, same shape as q, written.
- *   lse     : fp32 [batch][heads][seq_len] or NULL.  Must be non-NULL when
- *             acc != NULL (the pooled probabilities use it).
+ *   lse     : fp32 [batch][heads][seq_len] or NULL.
  *   acc     : fp32 [batch][heads][nb][nb] or NULL (plain dense attention).
- *             Read-modify-written; the caller zeroes it before the first
- *             step of the discovery window.  Each acc row is owned by one
- *             workgroup: no float atomics, bitwise deterministic.
- * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with lse NULL),
- *         WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_HIP.
+ *             Read-modify-written in the same pass as the attention: the
+ *             caller zeroes it before the first step it should sum.  Each
+ *             acc row is owned by one work-group: no float atomics, bitwise
+ *             deterministic.
+ *   workspace, workspace_bytes : device scratch of at least
+ *             wise_mass_workspace_bytes(s) bytes, 256-byte aligned, used
+ *             only when acc != NULL (then required); contents on entry are
+ *             ignored.  It holds one fp32 per (query, 64-key span, or 32-key
+ *             span for block 32) between the attention and its epilogue.
+ * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with workspace NULL),
+ *         WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_WORKSPACE, WISE_ERR_HIP.
  */
 wise_status wise_dense_attn_accum(const wise_shape* s, const void* q,
                                   const void* k, const void* v, void* o,
-                                  float* lse, float* acc, void* hip_stream);
+                                  float* lse, float* acc, void* workspace,
+                                  size_t workspace_bytes, void* hip_stream);
 
 /*
  * wise_select_support — per query block, the smallest set of key blocks whose
@@ -277,6 +285,11 @@ wise_status wise_support_mass(const wise_shape* s, const float* r,
                               const int32_t* row_ptr, const int32_t* col_idx,
                               double* row_mass, double* totals,
                               void* hip_stream);
+
+/* Bytes of device workspace wise_dense_attn_accum needs when it pools block
+ * masses: batch * heads * seq_len * (seq_len / E) * 4 with E = 32 for block
+ * 32 and 64 otherwise (0 for an invalid shape). */
+size_t wise_mass_workspace_bytes(const wise_shape* s);
 
 /* 64-bit words per row of a support bitmask: ceil(nb / 64)
  * (-1 for an invalid shape). */

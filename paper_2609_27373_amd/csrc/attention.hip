@@ -1,7 +1,9 @@
 // attention.hip — the two attention kernels of libwise on gfx950:
 //
 //   dense_attn_kernel   causal flash attention, O and natural-log LSE
-//                       (paper Section 3, eq. recurrent_attention)
+//                       (paper Section 3, eq. recurrent_attention), and
+//                       optionally the block-pooled attention mass
+//                       (Section 5.1, eq. block_attention_mass)
 //   sparse_attn_kernel  attention restricted to a CSR block support
 //                       (Section 5.2, eq. wise_attention)
 //
@@ -93,6 +95,7 @@ struct WaveRows {
   f32x16_t o[G::kDTiles];    // O^T accumulator, 32 dims x 32 queries per tile
   float m;                   // running max of scale*log2(e)*s (per query)
   float l;                   // running sum over this lane's half of the keys
+  float hs[2];               // last tile's per-half sums (softmax_pv<H, true>)
 
   __device__ __forceinline__ void load_q(const uint16_t* qg, int q0, int lane) {
     const uint16_t* row = qg + (size_t)(q0 + (lane & 31)) * D + 8 * (lane >> 5);
@@ -133,8 +136,10 @@ struct WaveRows {
         if (key0 + score_key(t, r, h) > qi) s[t][r] = -INFINITY;
   }
 
-  // Online softmax of one tile and O^T += V^T P^T.
-  template <int H>
+  // Online softmax of one tile and O^T += V^T P^T.  With kHalves the sums
+  // of this lane's probabilities over each 32-key half of the tile are kept
+  // in hs[] (the row sum then adds the halves).
+  template <int H, bool kHalves = false>
   __device__ __forceinline__ void softmax_pv(f32x16_t s[H], const uint16_t* vt, int lane, float c) {
     float mx = -INFINITY;
 #pragma unroll
@@ -164,11 +169,17 @@ struct WaveRows {
     float ts = 0.f;
 #pragma unroll
     for (int t = 0; t < H; ++t) {
+      float th = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[t][r], c, -mb));
         s[t][r] = p;
-        ts += p;
+        if constexpr (kHalves) th += p;
+        else ts += p;
+      }
+      if constexpr (kHalves) {
+        hs[t] = th;
+        ts += th;
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -194,7 +205,7 @@ struct WaveRows {
   // One tile: S^T, the causal mask when the tile reaches past this wave's
   // first query (only ever on diagonal tiles, and only instantiated for
   // them), online softmax and PV.
-  template <bool kMask, int H = 2>
+  template <bool kMask, int H = 2, bool kHalves = false>
   __device__ __forceinline__ void attend(const uint16_t* ks, const uint16_t* vt, int lane,
                                          float c, int key0, int q0) {
     f32x16_t s[H];
@@ -202,8 +213,28 @@ struct WaveRows {
     if constexpr (kMask) {
       if (key0 + 32 * H - 1 > q0) mask<H>(s, key0, q0 + (lane & 31), lane);
     }
-    softmax_pv<H>(s, vt, lane, c);
+    softmax_pv<H, kHalves>(s, vt, lane, c);
   }
+
+  // log2 of the last tile's probability mass per query, unnormalised (taken
+  // against the running max m): entry 0 and 1 for the two 32-key halves
+  // (E = 32) or entry 0 for the whole tile (E = 64).  -inf for no mass.
+  template <int E>
+  __device__ __forceinline__ void tile_log_mass(float out[2]) const {
+    if constexpr (E == 32) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const float x = pair_sum(hs[t]);
+        out[t] = x > 0.f ? m + __builtin_log2f(x) : -INFINITY;
+      }
+    } else {
+      const float x = pair_sum(hs[0] + hs[1]);
+      out[0] = x > 0.f ? m + __builtin_log2f(x) : -INFINITY;
+    }
+  }
+
+  // log2 of the row normaliser: lse / ln 2.
+  __device__ __forceinline__ float lse2() const { return m + __builtin_log2f(pair_sum(l)); }
 
   // O = O^T / l written as bf16 rows; lse in natural log.
   __device__ __forceinline__ void finish(uint16_t* og, float* lse, int q0, int lane) const {
@@ -227,14 +258,33 @@ struct WaveRows {
 // ---------------------------------------------------------------------------
 // Dense causal attention.  A work-group of NW waves owns 32*NW consecutive
 // queries of one (batch, head); heavier (later) query tiles are issued first.
+//
+// With BM > 0 the kernel also pools the attention mass into blocks of BM keys
+// and BM queries (Section 5.1, eq. block_attention_mass):
+//   acc[qb][kb] += (1/BM) sum_{i in qb} sum_{j in kb, j <= i} A_ij.
+// A_ij = 2^(s_ij - lse2_i) needs the row normaliser, known only after the
+// row's last tile, so every tile leaves per query the log2 of its
+// unnormalised mass (against the running max of that moment) in a workspace
+// entry of E = min(BM, 64) keys, and the epilogue, once lse2 is known, turns
+// each entry into 2^(entry - lse2), sums it over the wave's 32 queries and
+// then over the waves and entries of each (query block, key block).  The
+// group owns the acc rows of its query blocks: no atomics, and the sums run
+// in a fixed order, so the result is bitwise reproducible.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
+constexpr int kMassChunk = 256;   // workspace entries reduced per epilogue pass
+constexpr int kMassBatch = 16;    // entry loads in flight per half-wave in the epilogue
+
+template <int D, int NW, int BM>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-                  float* __restrict__ lse, int n, int heads, int gq, Sched sc, float c) {
+                  float* __restrict__ lse, int n, int heads, int gq, Sched sc, float c,
+                  float* __restrict__ acc, float* __restrict__ mws) {
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kQT = NW * 32;
+  constexpr bool kMass = BM > 0;
+  constexpr int kE = BM == 32 ? 32 : 64;            // keys per workspace entry
+  constexpr int kEPT = kKeyTile / kE;               // entries per 64-key tile
   __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
   __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
   int bh, item;
@@ -244,10 +294,23 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
+  const int nent = n / kE;                          // workspace entries per query
+  float* ew = kMass ? mws + (size_t)bh * nent * n + q0 + (lane & 31) : nullptr;
 
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
   w.reset();
+  // Per-tile mass entries of this lane's query (lanes 0..31 write them).
+  auto put_mass = [&](int it) {
+    if constexpr (kMass) {
+      float lm[2];
+      w.template tile_log_mass<kE>(lm);
+      if (lane < 32) {
+#pragma unroll
+        for (int t = 0; t < kEPT; ++t) ew[(size_t)(it * kEPT + t) * n] = lm[t];
+      }
+    }
+  };
   // Tiles 0 .. nfull-1 lie wholly below every query of the group; the last
   // kQT/64 tiles hold the diagonal and are masked per wave.
   const uint16_t* Kh = K + kvoff;
@@ -260,7 +323,8 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
     st.store(ks, vt, tid);
     __syncthreads();
     st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
-    w.template attend<false>(ks, vt, lane, c, it * kKeyTile, q0);
+    w.template attend<false, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+    put_mass(it);
     __syncthreads();
   }
   for (int it = nfull; it < ntiles; ++it) {
@@ -268,10 +332,60 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
     __syncthreads();
     if (it + 1 < ntiles)
       st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
-    if (it * kKeyTile <= q0) w.template attend<true>(ks, vt, lane, c, it * kKeyTile, q0);
+    if (it * kKeyTile <= q0) {
+      w.template attend<true, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+      put_mass(it);
+    }
     __syncthreads();
   }
   w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+  if constexpr (kMass) {
+    // Epilogue: entries 0 .. elast of this wave were written above (the
+    // tiles it attended); later ones hold no mass for its queries.
+    constexpr int kWPB = BM / 32;                   // waves per query block
+    constexpr int kQB = kQT / BM;                   // query blocks of the group
+    constexpr int kBE = BM / kE;                    // entries per key block
+    static_assert(kQB >= 1 && kQT % BM == 0, "mass block larger than the group");
+    __shared__ float red[NW][kMassChunk];
+    const float l2 = w.lse2();
+    const int elast = (q0 + 31) / kE;
+    const int nb = n / BM;
+    const int eend = (qbase + kQT - 1) / kE + 1;    // entries any wave of the group wrote
+    const int hsel = lane >> 5;                     // each half-wave takes every other entry
+    for (int c0 = 0; c0 < eend; c0 += kMassChunk) {
+      const int cend = min(c0 + kMassChunk, eend);
+      for (int e0 = c0; e0 < cend; e0 += 2 * kMassBatch) {
+        float x[kMassBatch];
+#pragma unroll
+        for (int u = 0; u < kMassBatch; ++u) {      // all loads first, then the sums
+          const int e = e0 + 2 * u + hsel;
+          x[u] = e < cend && e <= elast ? ew[(size_t)e * n] : -INFINITY;
+        }
+#pragma unroll
+        for (int u = 0; u < kMassBatch; ++u) {
+          float y = fast_exp2(x[u] - l2);
+#pragma unroll
+          for (int off = 16; off >= 1; off >>= 1) y += __shfl_xor(y, off, 64);
+          const int e = e0 + 2 * u + hsel;
+          if ((lane & 31) == 0 && e < cend) red[wave][e - c0] = y;
+        }
+      }
+      __syncthreads();
+      const int b0 = c0 / kBE, b1 = (min(c0 + kMassChunk, eend) + kBE - 1) / kBE;
+      for (int x = tid; x < kQB * (b1 - b0); x += kNT) {
+        const int j = x / (b1 - b0), kb = b0 + x % (b1 - b0);
+        const int qb = qbase / BM + j;
+        if (kb > qb) continue;
+        float sum = 0.f;
+#pragma unroll
+        for (int wv = 0; wv < kWPB; ++wv)
+#pragma unroll
+          for (int u = 0; u < kBE; ++u) sum += red[j * kWPB + wv][kb * kBE + u - c0];
+        acc[((size_t)bh * nb + qb) * nb + kb] += sum * (1.f / BM);
+      }
+      __syncthreads();
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -356,33 +470,48 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // Launchers (shapes already validated by the C ABI layer).
 // ---------------------------------------------------------------------------
+template <int D, int NW, int BM>
+static void launch_dense_nw(const Dims& s, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            uint16_t* O, float* lse, float* acc, float* ws, hipStream_t st) {
+  const Sched sc = make_sched(s.bh, s.n / (NW * 32), (size_t)s.n * D * 4 / s.gq);
+  hipLaunchKernelGGL((dense_attn_kernel<D, NW, BM>), dim3(sched_grid(sc)), dim3(NW * 64), 0, st,
+                     Q, K, V, O, lse, s.n, s.heads, s.gq, sc, s.scale * kLog2e, acc, ws);
+}
+
+template <int D, int NW>
+static void launch_dense_bm(const Dims& s, const uint16_t* Q, const uint16_t* K,
+                            const uint16_t* V, uint16_t* O, float* lse, float* acc, float* ws,
+                            hipStream_t st) {
+  if (acc == nullptr) return launch_dense_nw<D, NW, 0>(s, Q, K, V, O, lse, acc, ws, st);
+  if (s.block == 32) return launch_dense_nw<D, NW, 32>(s, Q, K, V, O, lse, acc, ws, st);
+  if (s.block == 64) return launch_dense_nw<D, NW, 64>(s, Q, K, V, O, lse, acc, ws, st);
+  if constexpr (NW == 4) launch_dense_nw<D, NW, 128>(s, Q, K, V, O, lse, acc, ws, st);
+}
+
 template <int D>
 static hipError_t launch_dense_d(const Dims& s, const void* q, const void* k, const void* v,
-                                 void* o, float* lse, hipStream_t st) {
-  const float c = s.scale * kLog2e;
+                                 void* o, float* lse, float* acc, float* ws, hipStream_t st) {
   const auto* Q = (const uint16_t*)q;
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
-  const size_t kv = (size_t)s.n * D * 4 / s.gq;   // K/V bytes per query head
-  if (s.n % 128 == 0) {
-    const Sched sc = make_sched(s.bh, s.n / 128, kv);
-    hipLaunchKernelGGL((dense_attn_kernel<D, 4>), dim3(sched_grid(sc)), dim3(256), 0, st, Q, K,
-                       V, (uint16_t*)o, lse, s.n, s.heads, s.gq, sc, c);
-  } else {
-    const Sched sc = make_sched(s.bh, s.n / 64, kv);
-    hipLaunchKernelGGL((dense_attn_kernel<D, 2>), dim3(sched_grid(sc)), dim3(128), 0, st, Q, K,
-                       V, (uint16_t*)o, lse, s.n, s.heads, s.gq, sc, c);
-  }
+  // 128 queries per group when they divide n (always so for 128-key blocks).
+  if (s.n % 128 == 0) launch_dense_bm<D, 4>(s, Q, K, V, (uint16_t*)o, lse, acc, ws, st);
+  else launch_dense_bm<D, 2>(s, Q, K, V, (uint16_t*)o, lse, acc, ws, st);
   return hipGetLastError();
 }
 
 hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void* v, void* o,
-                        float* lse, hipStream_t st) {
+                        float* lse, float* acc, void* ws, hipStream_t st) {
   switch (s.d) {
-    case 64: return launch_dense_d<64>(s, q, k, v, o, lse, st);
-    case 96: return launch_dense_d<96>(s, q, k, v, o, lse, st);
-    default: return launch_dense_d<128>(s, q, k, v, o, lse, st);
+    case 64: return launch_dense_d<64>(s, q, k, v, o, lse, acc, (float*)ws, st);
+    case 96: return launch_dense_d<96>(s, q, k, v, o, lse, acc, (float*)ws, st);
+    default: return launch_dense_d<128>(s, q, k, v, o, lse, acc, (float*)ws, st);
   }
+}
+
+size_t mass_workspace_bytes(const Dims& s) {
+  const size_t e = s.block == 32 ? 32 : 64;
+  return (size_t)s.bh * (s.n / e) * s.n * sizeof(float);
 }
 
 template <int D>

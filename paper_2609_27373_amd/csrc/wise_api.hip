@@ -57,18 +57,19 @@ wise_status from_hip(hipError_t e) { return e == hipSuccess ? WISE_OK : WISE_ERR
 extern "C" {
 
 wise_status wise_dense_attn_accum(const wise_shape* s, const void* q, const void* k,
-                                  const void* v, void* o, float* lse, float* acc,
-                                  void* hip_stream) {
+                                  const void* v, void* o, float* lse, float* acc, void* workspace,
+                                  size_t workspace_bytes, void* hip_stream) {
   wise::Dims d;
   wise_status st = check_shape(s, &d);
   if (st != WISE_OK) return st;
   if ((st = check_qkvo(q, k, v, o)) != WISE_OK) return st;
-  if (acc != nullptr && lse == nullptr) return WISE_ERR_NULL;
-  if ((lse && !aligned(lse, 4)) || (acc && !aligned(acc, 4))) return WISE_ERR_SHAPE;
-  const hipStream_t stream = (hipStream_t)hip_stream;
-  hipError_t e = wise::launch_dense(d, q, k, v, o, lse, stream);
-  if (e == hipSuccess && acc != nullptr) e = wise::launch_mass(d, q, k, lse, acc, stream);
-  return from_hip(e);
+  if (acc != nullptr && workspace == nullptr) return WISE_ERR_NULL;
+  if ((lse && !aligned(lse, 4)) || (acc && !aligned(acc, 4)) ||
+      (acc && !aligned(workspace, 256)))
+    return WISE_ERR_SHAPE;
+  if (acc != nullptr && workspace_bytes < wise::mass_workspace_bytes(d)) return WISE_ERR_WORKSPACE;
+  return from_hip(wise::launch_dense(d, q, k, v, o, lse, acc, acc ? workspace : nullptr,
+                                     (hipStream_t)hip_stream));
 }
 
 wise_status wise_select_support(const wise_shape* s, const float* acc, float tau, uint32_t flags,
@@ -169,6 +170,12 @@ wise_status wise_support_mass(const wise_shape* s, const float* r, const int32_t
     return WISE_ERR_SHAPE;
   return from_hip(wise::launch_support_mass(d, r, row_ptr, col_idx, row_mass, totals,
                                             (hipStream_t)hip_stream));
+}
+
+size_t wise_mass_workspace_bytes(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return 0;
+  return wise::mass_workspace_bytes(d);
 }
 
 int32_t wise_mask_words(const wise_shape* s) {

@@ -18,9 +18,8 @@ struct Dims {
 constexpr int kMaxSelectBlocks = 1024;  // selection keeps a row's candidates in LDS
 
 hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void* v, void* o,
-                        float* lse, hipStream_t st);
-hipError_t launch_mass(const Dims& s, const void* q, const void* k, const float* lse, float* acc,
-                       hipStream_t st);
+                        float* lse, float* acc, void* ws, hipStream_t st);
+size_t mass_workspace_bytes(const Dims& s);
 hipError_t launch_sparse(const Dims& s, const void* q, const void* k, const void* v,
                          const int32_t* row_ptr, const int32_t* col_idx, const int32_t* order,
                          void* o, float* lse, hipStream_t st);

@@ -26,7 +26,8 @@ from . import wise
 
 def retained_mass(shape, q, k, v, schedule, scratch=None):
     """(fraction, row_mass) of one step's full-attention mass inside the
-    support held by `schedule`.  `scratch` may supply (o, lse, r) buffers."""
+    support held by `schedule`.  `scratch` may supply (o, lse, r, workspace)
+    buffers."""
     bh = shape.batch * shape.heads
     nb = shape.seq_len // shape.block
     dev = q.device
@@ -35,10 +36,11 @@ def retained_mass(shape, q, k, v, schedule, scratch=None):
                    torch.empty((shape.batch, shape.heads, shape.seq_len), dtype=torch.float32,
                                device=dev),
                    torch.empty((shape.batch, shape.heads, nb, nb), dtype=torch.float32,
-                               device=dev))
-    o, lse, r = scratch
+                               device=dev),
+                   wise.mass_workspace(shape, dev))
+    o, lse, r, ws = scratch
     r.zero_()
-    wise.wise_dense_attn_accum(shape, q, k, v, o, lse, r)
+    wise.wise_dense_attn_accum(shape, q, k, v, o, lse, r, ws)
     row_mass = torch.empty((bh * nb, 2), dtype=torch.float64, device=dev)
     totals = torch.empty(2, dtype=torch.float64, device=dev)
     wise.wise_support_mass(shape, r, schedule.row_ptr, schedule.col_idx, row_mass, totals)
@@ -65,6 +67,7 @@ class RollingSets:
                              device=device)
         self.lse = torch.empty((shape.batch, shape.heads, shape.seq_len), dtype=torch.float32,
                                device=device)
+        self.ws = wise.mass_workspace(shape, device)
         self.t = 0
 
     def step(self, q, k, v, o):
@@ -72,7 +75,7 @@ class RollingSets:
         |W^(t-1) | W^(t)|) for t >= 2, None for t = 1."""
         self.t += 1
         self.r.zero_()
-        wise.wise_dense_attn_accum(self.shape, q, k, v, o, self.lse, self.r)
+        wise.wise_dense_attn_accum(self.shape, q, k, v, o, self.lse, self.r, self.ws)
         wise.wise_select_step(self.shape, self.r, self.tau, self.ring[(self.t - 1) % self.width])
         self.prev.copy_(self.cur)
         wise.wise_mask_union(self.shape, self.ring, min(self.t, self.width), self.cur)

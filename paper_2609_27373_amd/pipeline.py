@@ -41,6 +41,7 @@ class WisePipeline:
         self.acc = torch.zeros((batch, heads, nb, nb), dtype=torch.float32, device=device)
         self.lse = torch.empty((batch, heads, seq_len), dtype=torch.float32, device=device)
         self.schedule = wise.Schedule(self.shape, device)
+        self.mass_ws = wise.mass_workspace(self.shape, device)
         self.window = int(window)
         self.masks = None
         if mode == "union":
@@ -64,12 +65,13 @@ class WisePipeline:
             if self.filled >= self.window:
                 raise RuntimeError("more window steps than the union window holds")
             self.acc.zero_()
-            wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse, self.acc)
+            wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse, self.acc, self.mass_ws)
             wise.wise_select_step(self.shape, self.acc, self.tau, self.masks[self.filled])
             self.filled += 1
         else:
             wise.wise_dense_attn_accum(self.shape, q, k, v, out, self.lse,
-                                       self.acc if accumulate else None)
+                                       self.acc if accumulate else None,
+                                       self.mass_ws if accumulate else None)
         return out
 
     def dense_step(self, q, k, v, out, lse=None):

@@ -28,7 +28,8 @@ STATUS_NAMES = {0: "WISE_OK", 1: "WISE_ERR_NULL", 2: "WISE_ERR_SHAPE", 3: "WISE_
 # Every symbol include/wise.h declares.
 EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_sparse_attn",
            "wise_select_step", "wise_support_from_masks", "wise_mask_union", "wise_mask_overlap",
-           "wise_support_mass", "wise_mask_words", "wise_select_workspace_bytes",
+           "wise_support_mass", "wise_mass_workspace_bytes", "wise_mask_words",
+           "wise_select_workspace_bytes",
            "wise_support_capacity", "wise_status_string", "wise_abi_version")
 
 
@@ -71,7 +72,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     S = ctypes.POINTER(wise_shape)
-    lib.wise_dense_attn_accum.argtypes = [S, P, P, P, P, P, P, P]
+    lib.wise_dense_attn_accum.argtypes = [S, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     lib.wise_dense_attn_accum.restype = ctypes.c_int
     lib.wise_select_support.argtypes = [S, P, ctypes.c_float, ctypes.c_uint32, P, P, P, P,
                                         ctypes.c_size_t, P]
@@ -89,6 +90,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wise_mask_overlap.restype = ctypes.c_int
     lib.wise_support_mass.argtypes = [S, P, P, P, P, P, P]
     lib.wise_support_mass.restype = ctypes.c_int
+    lib.wise_mass_workspace_bytes.argtypes = [S]
+    lib.wise_mass_workspace_bytes.restype = ctypes.c_size_t
     lib.wise_mask_words.argtypes = [S]
     lib.wise_mask_words.restype = ctypes.c_int32
     lib.wise_select_workspace_bytes.argtypes = [S]
@@ -142,14 +145,24 @@ def _kv_numel(s: wise_shape) -> int:
     return s.batch * (s.kv_heads or s.heads) * s.seq_len * s.head_dim
 
 
-def wise_dense_attn_accum(s: wise_shape, q, k, v, o, lse=None, acc=None, stream=None) -> None:
+def wise_dense_attn_accum(s: wise_shape, q, k, v, o, lse=None, acc=None, workspace=None,
+                          stream=None) -> None:
+    """`workspace` (any dtype, at least wise_mass_workspace_bytes(s) bytes)
+    is required with `acc`; mass_workspace() allocates one."""
     nqkv, nlse, nacc, _ = _sizes(s)
     nkv = _kv_numel(s)
     bf = torch.bfloat16
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(_lib().wise_dense_attn_accum(
         ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nkv), _ptr(v, bf, "v", nkv),
         _ptr(o, bf, "o", nqkv), _ptr(lse, torch.float32, "lse", nlse),
-        _ptr(acc, torch.float32, "acc", nacc), _stream(stream)), "wise_dense_attn_accum")
+        _ptr(acc, torch.float32, "acc", nacc), _ptr(workspace, None, "workspace"),
+        ctypes.c_size_t(ws_bytes), _stream(stream)), "wise_dense_attn_accum")
+
+
+def mass_workspace(s: wise_shape, device="cuda") -> torch.Tensor:
+    """A device buffer of wise_mass_workspace_bytes(s) bytes."""
+    return torch.empty(max(wise_mass_workspace_bytes(s), 1), dtype=torch.uint8, device=device)
 
 
 def wise_select_support(s: wise_shape, acc, tau: float, flags: int, row_ptr, col_idx,
@@ -223,6 +236,10 @@ def wise_support_mass(s: wise_shape, r, row_ptr, col_idx, row_mass, totals=None,
         ctypes.byref(s), _ptr(r, torch.float32, "r", nacc), _ptr(row_ptr, i32, "row_ptr", rows + 1),
         _ptr(col_idx, i32, "col_idx"), _ptr(row_mass, f64, "row_mass", 2 * rows),
         _ptr(totals, f64, "totals", 2), _stream(stream)), "wise_support_mass")
+
+
+def wise_mass_workspace_bytes(s: wise_shape) -> int:
+    return int(_lib().wise_mass_workspace_bytes(ctypes.byref(s)))
 
 
 def wise_mask_words(s: wise_shape) -> int:

@@ -64,6 +64,9 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_support_capacity(S(seq_len=500)) == -1
     assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_support_capacity(S(block=32)) == 2 * 16 * 17 // 2
+    assert wise.wise_mass_workspace_bytes(S()) == 2 * 512 * (512 // 64) * 4
+    assert wise.wise_mass_workspace_bytes(S(block=32)) == 2 * 512 * (512 // 32) * 4
+    assert wise.wise_mass_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_mask_words(S()) == 1
     assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
     assert wise.wise_mask_words(s4) == 4
@@ -74,9 +77,9 @@ FAKE = ctypes.c_void_p(4096)        # aligned, never dereferenced: calls fail va
 MIS = ctypes.c_void_p(4096 + 2)     # misaligned
 
 
-def dense(lib, s, q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, acc=None):
+def dense(lib, s, q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, acc=None, ws=None, wsb=0):
     return lib.wise_dense_attn_accum(ctypes.byref(s) if s is not None else None, q, k, v, o, lse,
-                                     acc, None)
+                                     acc, ws, wsb, None)
 
 
 def select(lib, s, acc=FAKE, tau=0.9, flags=3, rp=FAKE, ci=FAKE, ro=None, ws=FAKE, wsb=1 << 30):
@@ -91,6 +94,7 @@ def sparse(lib, s, q=FAKE, rp=FAKE, ci=FAKE, o=FAKE):
 
 @pytest.mark.parametrize("case,status", [
     (dict(s=None), 1), (dict(q=None), 1), (dict(o=None), 1), (dict(acc=FAKE), 1),
+    (dict(acc=FAKE, ws=FAKE, wsb=16), 5), (dict(acc=FAKE, ws=ctypes.c_void_p(4096 + 16), wsb=1 << 40), 2),
     (dict(s=S(seq_len=500)), 2), (dict(s=S(batch=0)), 2), (dict(s=S(heads=-1)), 2),
     (dict(s=S(head_dim=80)), 3), (dict(s=S(block=16)), 3), (dict(q=MIS), 2),
     (dict(s=S(block=32, seq_len=96)), 2), (dict(s=S(block=256)), 3),

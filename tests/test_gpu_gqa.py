@@ -38,7 +38,7 @@ def test_gqa_dense_mass_sparse(gpu_lib, bt, h, kvh, n, d, B):
     lse = torch.empty((bt, h, n), device="cuda")
     acc = torch.zeros((bt, h, nb, nb), device="cuda")
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
-    w.wise_dense_attn_accum(s, qd, kd, vd, o, lse, acc)
+    w.wise_dense_attn_accum(s, qd, kd, vd, o, lse, acc, w.mass_workspace(s))
     torch.cuda.synchronize()
     o_ref, l_ref = O.dense_attention(qe, ke, ve)
     assert_attn(o, o_ref, "gqa dense O")
@@ -72,7 +72,7 @@ def test_explicit_kv_heads_equal_heads_is_plain_attention(gpu_lib):
         o = torch.empty_like(q)
         lse = torch.empty((bt, h, n), device="cuda")
         acc = torch.zeros((bt, h, n // B, n // B), device="cuda")
-        w.wise_dense_attn_accum(s, q, k, v, o, lse, acc)
+        w.wise_dense_attn_accum(s, q, k, v, o, lse, acc, w.mass_workspace(s))
         outs.append((o, lse, acc))
     torch.cuda.synchronize()
     for a, b in zip(*outs):

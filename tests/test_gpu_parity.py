@@ -69,7 +69,7 @@ def test_dense_and_mass(gpu_lib, bt, h, n, d, B):
     lse = torch.empty((bt, h, n), device="cuda")
     nb = n // B
     acc = torch.full((bt, h, nb, nb), 0.25, device="cuda")   # RMW onto a non-zero start
-    w.wise_dense_attn_accum(s, q.cuda(), k.cuda(), v.cuda(), o, lse, acc)
+    w.wise_dense_attn_accum(s, q.cuda(), k.cuda(), v.cuda(), o, lse, acc, w.mass_workspace(s))
     torch.cuda.synchronize()
     o_ref, l_ref = O.dense_attention(f64(q), f64(k), f64(v))
     assert_attn(o, o_ref, "dense O")
