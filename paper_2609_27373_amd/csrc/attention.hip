@@ -53,15 +53,18 @@ struct TileStage {
     return kChunks % NT == 0 || chunk(tid, i) < kChunks;
   }
 
-  // kt, vt: this tile's first key row (uniform); per-lane offsets are 32-bit.
-  __device__ __forceinline__ void load(const uint16_t* kt, const uint16_t* vt, int tid) {
+  // rk, rv: the head's K and V; key0: this tile's first key row (uniform,
+  // a scalar byte offset), per-lane offsets constant across tiles.
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                       int key0, int tid) {
+    const uint32_t soff = (uint32_t)key0 * (D * 2);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       if (live(tid, i)) {
         const int ch = chunk(tid, i);
-        const uint32_t off = (uint32_t)((ch / kRowChunks) * D + (ch % kRowChunks) * 8);
-        kr[i] = *(const u32x4_t*)(kt + off);
-        if constexpr (kWithV) vr[i] = *(const u32x4_t*)(vt + off);
+        const uint32_t off = (uint32_t)((ch / kRowChunks) * D + (ch % kRowChunks) * 8) * 2;
+        kr[i] = buffer_load16(rk, off, soff);
+        if constexpr (kWithV) vr[i] = buffer_load16(rv, off, soff);
       }
     }
   }
@@ -313,16 +316,15 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   };
   // Tiles 0 .. nfull-1 lie wholly below every query of the group; the last
   // kQT/64 tiles hold the diagonal and are masked per wave.
-  const uint16_t* Kh = K + kvoff;
-  const uint16_t* Vh = V + kvoff;
+  const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
   const int ntiles = (qbase + kQT) / kKeyTile;
   const int nfull = qbase / kKeyTile;
   TileStage<D, kNT, true> st;
-  st.load(Kh, Vh, tid);
+  st.load(rk, rv, 0, tid);
   for (int it = 0; it < nfull; ++it) {
     st.store(ks, vt, tid);
     __syncthreads();
-    st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
+    st.load(rk, rv, (it + 1) * kKeyTile, tid);
     w.template attend<false, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
     put_mass(it);
     __syncthreads();
@@ -330,8 +332,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   for (int it = nfull; it < ntiles; ++it) {
     st.store(ks, vt, tid);
     __syncthreads();
-    if (it + 1 < ntiles)
-      st.load(Kh + (size_t)(it + 1) * kKeyTile * D, Vh + (size_t)(it + 1) * kKeyTile * D, tid);
+    if (it + 1 < ntiles) st.load(rk, rv, (it + 1) * kKeyTile, tid);
     if (it * kKeyTile <= q0) {
       w.template attend<true, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
       put_mass(it);
@@ -420,8 +421,7 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int beg = row_ptr[row];
   const int nent = row_ptr[row + 1] - beg;
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
-  const uint16_t* Kh = K + kvoff;
-  const uint16_t* Vh = V + kvoff;
+  const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
 
   // Tile it of the row: entry it / kTPB, sub-tile it % kTPB.  Ids outside
   // 0..qb are skipped (their tile is never loaded out of bounds nor used).
@@ -441,13 +441,13 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int nfull = (nent - 1) * kTPB;
   bool ok = false;
   int key0 = ntiles > 0 ? tile_key(0, ok) : 0;
-  if (ntiles > 0) st.load(Kh + (size_t)key0 * D, Vh + (size_t)key0 * D, tid);
+  if (ntiles > 0) st.load(rk, rv, key0, tid);
   for (int it = 0; it < nfull; ++it) {
     st.store(ks, vt, tid);
     __syncthreads();
     bool ok_next;
     const int key_next = tile_key(it + 1, ok_next);
-    st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
+    st.load(rk, rv, key_next, tid);
     if (ok && key0 + KT - 1 < qb * kB) w.template attend<false, kH>(ks, vt, lane, c, key0, q0);
     __syncthreads();
     key0 = key_next;
@@ -458,7 +458,7 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
     __syncthreads();
     bool ok_next = false;
     const int key_next = (it + 1 < ntiles) ? tile_key(it + 1, ok_next) : 0;
-    if (it + 1 < ntiles) st.load(Kh + (size_t)key_next * D, Vh + (size_t)key_next * D, tid);
+    if (it + 1 < ntiles) st.load(rk, rv, key_next, tid);
     if (ok && key0 <= q0) w.template attend<true, kH>(ks, vt, lane, c, key0, q0);
     __syncthreads();
     key0 = key_next;

@@ -39,6 +39,17 @@ __device__ __forceinline__ u32x2_t lds_read_tr16(const uint16_t* p) {
   return __builtin_bit_cast(u32x2_t, r);
 }
 
+// Buffer resource over `base` for raw 16-byte loads (32-bit byte offsets:
+// the head's base stays in scalar registers and a tile needs no 64-bit
+// address arithmetic per lane).  Offsets past num_records read as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ u32x4_t buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                 uint32_t soff) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
 // Two fp32 -> packed bf16x2 (round to nearest even), lo in bits 0..15.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   f32x2_t v = {lo, hi};
