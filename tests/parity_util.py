@@ -69,3 +69,33 @@ def compare_support(gpu_rows, acc_ref, tau, flags, row_ids=None):
     return reported
 
 
+
+
+def check_csr(rp, ci, nb, flags):
+    """Properties every selected CSR has, checked on the GPU's output alone:
+    row_ptr non-decreasing from 0, ids ascending within 0..qb, forced blocks
+    present, no empty row."""
+    rp = np.asarray(rp)
+    ci = np.asarray(ci)
+    assert rp[0] == 0 and np.all(np.diff(rp) >= 1) and rp[-1] == ci.size
+    for r in range(rp.size - 1):
+        row = ci[rp[r]:rp[r + 1]]
+        qb = r % nb
+        assert np.all(np.diff(row) > 0) and row[0] >= 0 and row[-1] <= qb, f"row {r}: {row}"
+        if flags & 1:
+            assert row[0] == 0, f"row {r}: sink missing"
+        if flags & 2:
+            assert row[-1] == qb, f"row {r}: diagonal missing"
+
+
+def check_row_order(order, rp, nb):
+    """row_order is a permutation that keeps each head's rows in the head's
+    own nb slots, longest support first, ties by row id."""
+    order = np.asarray(order)
+    cnt = np.diff(np.asarray(rp))
+    assert np.array_equal(np.sort(order), np.arange(order.size))
+    for h in range(order.size // nb):
+        seg = order[h * nb:(h + 1) * nb]
+        assert np.all(seg // nb == h)
+        c = cnt[seg]
+        assert np.all((c[:-1] > c[1:]) | ((c[:-1] == c[1:]) & (seg[:-1] < seg[1:])))
