@@ -8,7 +8,8 @@
 //                       (Section 5.2, eq. wise_attention)
 //
 // Shared tile engine.  A wave owns 32 consecutive queries.  For each tile of
-// 64 keys it computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K from
+// 64 keys (32 for 32-key blocks) it computes S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16 (A = K from
 // LDS, B = Q^T held in registers for the whole row), so every lane ends up
 // holding 32 scores of ONE query.  The row max needs one cross-lane step
 // (lanes l and l^32 share a query), the row sum none until the end, and the

@@ -1,6 +1,6 @@
-// wise_device.hpp — gfx950 device helpers shared by the libwise kernels:
-// vector types, the bf16 MFMA wrapper, packing, cross-lane helpers and the
-// tile geometry of the attention kernels.
+// wise_device.hpp — gfx950 device helpers of the libwise attention kernels:
+// vector types, the bf16 MFMA wrapper, buffer loads, packing, cross-lane
+// helpers, the tile geometry and the work order.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -16,9 +16,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kWave = 64;
 constexpr int kKeyTile = 64;    // keys per LDS tile
-constexpr int kQPerWave = 32;   // queries owned by one wave (MFMA N dimension)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -73,21 +71,6 @@ __device__ __forceinline__ float pair_sum(float x) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Interleave the bf16 halves of two dwords: (lo(a), lo(b)) or (hi(a), hi(b)).
-__device__ __forceinline__ uint32_t lo_halves(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x05040100u);
-}
-__device__ __forceinline__ uint32_t hi_halves(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x07060302u);
-}
-
-// Full-wave fp32 sum in a fixed butterfly order (deterministic).
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-  return x;
-}
 
 // Tile geometry of the attention kernels for head dimension D.
 template <int D>
