@@ -121,7 +121,8 @@ enum {
  *             wise_mass_workspace_bytes(s) bytes, 256-byte aligned, used
  *             only when acc != NULL (then required); contents on entry are
  *             ignored.  It holds one fp32 per (query, 64-key span, or 32-key
- *             span for block 32) between the attention and its epilogue.
+ *             span for block 32, up to the query's tile) between the
+ *             attention and its epilogue.
  * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with workspace NULL),
  *         WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_WORKSPACE, WISE_ERR_HIP.
  */
@@ -287,8 +288,11 @@ wise_status wise_support_mass(const wise_shape* s, const float* r,
                               void* hip_stream);
 
 /* Bytes of device workspace wise_dense_attn_accum needs when it pools block
- * masses: batch * heads * seq_len * (seq_len / E) * 4 with E = 32 for block
- * 32 and 64 otherwise (0 for an invalid shape). */
+ * masses: one fp32 per (query, E-key span up to the end of its tile of T
+ * queries), E = 32 for block 32 and 64 otherwise, T = 128 when it divides
+ * seq_len and 64 otherwise: batch * heads * T * (T / E) * m (m + 1) / 2 * 4
+ * with m = seq_len / T (about half of seq_len^2 / E floats per head; 0 for
+ * an invalid shape). */
 size_t wise_mass_workspace_bytes(const wise_shape* s);
 
 /* 64-bit words per row of a support bitmask: ceil(nb / 64)

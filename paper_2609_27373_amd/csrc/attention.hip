@@ -269,7 +269,8 @@ struct WaveRows {
 // A_ij = 2^(s_ij - lse2_i) needs the row normaliser, known only after the
 // row's last tile, so every tile leaves per query the log2 of its
 // unnormalised mass (against the running max of that moment) in a workspace
-// entry of E = min(BM, 64) keys, and the epilogue, once lse2 is known, turns
+// entry of E = min(BM, 64) keys (only spans up to the query tile's end are
+// stored), and the epilogue, once lse2 is known, turns
 // each entry into 2^(entry - lse2), sums it over the wave's 32 queries and
 // then over the waves and entries of each (query block, key block).  The
 // group owns the acc rows of its query blocks: no atomics, and the sums run
@@ -298,8 +299,13 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
-  const int nent = n / kE;                          // workspace entries per query
-  float* ew = kMass ? mws + (size_t)bh * nent * n + q0 + (lane & 31) : nullptr;
+  // Workspace: per head, per query tile qt, (qt+1)*kQT/kE entries of kQT
+  // queries each (only the spans up to the tile's last query), query-minor.
+  const int nq = sc.items;
+  const size_t per_tile = (size_t)kQT * (kQT / kE);
+  float* ew = kMass ? mws + per_tile * ((size_t)bh * nq * (nq + 1) / 2 + (size_t)qt * (qt + 1) / 2) +
+                          32 * wave + (lane & 31)
+                    : nullptr;
 
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
@@ -311,7 +317,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
       w.template tile_log_mass<kE>(lm);
       if (lane < 32) {
 #pragma unroll
-        for (int t = 0; t < kEPT; ++t) ew[(size_t)(it * kEPT + t) * n] = lm[t];
+        for (int t = 0; t < kEPT; ++t) ew[(size_t)(it * kEPT + t) * kQT] = lm[t];
       }
     }
   };
@@ -361,7 +367,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
 #pragma unroll
         for (int u = 0; u < kMassBatch; ++u) {      // all loads first, then the sums
           const int e = e0 + 2 * u + hsel;
-          x[u] = e < cend && e <= elast ? ew[(size_t)e * n] : -INFINITY;
+          x[u] = e < cend && e <= elast ? ew[(size_t)e * kQT] : -INFINITY;
         }
 #pragma unroll
         for (int u = 0; u < kMassBatch; ++u) {
@@ -511,8 +517,12 @@ hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void*
 }
 
 size_t mass_workspace_bytes(const Dims& s) {
+  // Matches dense_attn_kernel: kQT-query tiles (128 when they divide n),
+  // entries of E keys, tile qt holding (qt+1)*kQT/E entries of kQT queries.
   const size_t e = s.block == 32 ? 32 : 64;
-  return (size_t)s.bh * (s.n / e) * s.n * sizeof(float);
+  const size_t qt = s.n % 128 == 0 ? 128 : 64;
+  const size_t nq = s.n / qt;
+  return (size_t)s.bh * qt * (qt / e) * (nq * (nq + 1) / 2) * sizeof(float);
 }
 
 template <int D>

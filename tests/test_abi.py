@@ -64,8 +64,10 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_support_capacity(S(seq_len=500)) == -1
     assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_support_capacity(S(block=32)) == 2 * 16 * 17 // 2
-    assert wise.wise_mass_workspace_bytes(S()) == 2 * 512 * (512 // 64) * 4
-    assert wise.wise_mass_workspace_bytes(S(block=32)) == 2 * 512 * (512 // 32) * 4
+    # 512 = 4 tiles of 128 queries; tile t keeps (t+1)*2 spans of 64 keys (4 of 32 keys)
+    assert wise.wise_mass_workspace_bytes(S()) == 2 * 128 * 2 * (4 * 5 // 2) * 4
+    assert wise.wise_mass_workspace_bytes(S(block=32)) == 2 * 128 * 4 * (4 * 5 // 2) * 4
+    assert wise.wise_mass_workspace_bytes(S(seq_len=320)) == 2 * 64 * 1 * (5 * 6 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_mask_words(S()) == 1
     assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
