@@ -289,10 +289,10 @@ wise_status wise_support_mass(const wise_shape* s, const float* r,
 
 /* Bytes of device workspace wise_dense_attn_accum needs when it pools block
  * masses: one fp32 per (query, E-key span up to the end of its tile of T
- * queries), E = 32 for block 32 and 64 otherwise, T = 128 when it divides
- * seq_len and 64 otherwise: batch * heads * T * (T / E) * m (m + 1) / 2 * 4
- * with m = seq_len / T (about half of seq_len^2 / E floats per head; 0 for
- * an invalid shape). */
+ * queries), E = 32 for block 32 and 64 otherwise, T = 256 for head_dim 128
+ * when it divides seq_len, else 128 when it divides seq_len, else 64:
+ * batch * heads * T * (T / E) * m (m + 1) / 2 * 4 with m = seq_len / T
+ * (about half of seq_len^2 / E floats per head; 0 for an invalid shape). */
 size_t wise_mass_workspace_bytes(const wise_shape* s);
 
 /* 64-bit words per row of a support bitmask: ceil(nb / 64)

@@ -20,6 +20,7 @@ constexpr int kMaxSelectBlocks = 1024;  // selection keeps a row's candidates in
 hipError_t launch_dense(const Dims& s, const void* q, const void* k, const void* v, void* o,
                         float* lse, float* acc, void* ws, hipStream_t st);
 size_t mass_workspace_bytes(const Dims& s);
+int dense_query_tile(const Dims& s);   // queries per dense work-group: 64, 128 or 256
 hipError_t launch_sparse(const Dims& s, const void* q, const void* k, const void* v,
                          const int32_t* row_ptr, const int32_t* col_idx, const int32_t* order,
                          void* o, float* lse, hipStream_t st);

@@ -68,6 +68,9 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_mass_workspace_bytes(S()) == 2 * 128 * 2 * (4 * 5 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(block=32)) == 2 * 128 * 4 * (4 * 5 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(seq_len=320)) == 2 * 64 * 1 * (5 * 6 // 2) * 4
+    # head_dim 128: tiles of 256 queries when they divide seq_len
+    assert wise.wise_mass_workspace_bytes(S(head_dim=128)) == 2 * 256 * 4 * (2 * 3 // 2) * 4
+    assert wise.wise_mass_workspace_bytes(S(head_dim=128, seq_len=384)) == 2 * 128 * 2 * (3 * 4 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_mask_words(S()) == 1
     assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
