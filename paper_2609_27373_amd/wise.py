@@ -165,6 +165,12 @@ def mass_workspace(s: wise_shape, device="cuda") -> torch.Tensor:
     return torch.empty(max(wise_mass_workspace_bytes(s), 1), dtype=torch.uint8, device=device)
 
 
+def _capacity(s: wise_shape) -> int:
+    """Entries col_idx must hold for a selection to write (0 for an invalid
+    shape, which the library then rejects)."""
+    return max(wise_support_capacity(s), 0)
+
+
 def wise_select_support(s: wise_shape, acc, tau: float, flags: int, row_ptr, col_idx,
                         row_order=None, workspace=None, stream=None) -> None:
     _, _, nacc, rows = _sizes(s)
@@ -173,7 +179,7 @@ def wise_select_support(s: wise_shape, acc, tau: float, flags: int, row_ptr, col
     _check(_lib().wise_select_support(
         ctypes.byref(s), _ptr(acc, torch.float32, "acc", nacc), ctypes.c_float(tau),
         ctypes.c_uint32(flags), _ptr(row_ptr, i32, "row_ptr", rows + 1),
-        _ptr(col_idx, i32, "col_idx"), _ptr(row_order, i32, "row_order", rows),
+        _ptr(col_idx, i32, "col_idx", _capacity(s)), _ptr(row_order, i32, "row_order", rows),
         _ptr(workspace, None, "workspace"), ctypes.c_size_t(ws_bytes), _stream(stream)),
         "wise_select_support")
 
@@ -209,7 +215,7 @@ def wise_support_from_masks(s: wise_shape, masks, n_masks: int, flags: int, row_
     _check(_lib().wise_support_from_masks(
         ctypes.byref(s), _ptr(masks, torch.int64, "masks", _mask_elems(s, max(n_masks, 0))),
         ctypes.c_int32(n_masks), ctypes.c_uint32(flags), _ptr(row_ptr, i32, "row_ptr", rows + 1),
-        _ptr(col_idx, i32, "col_idx"), _ptr(row_order, i32, "row_order", rows),
+        _ptr(col_idx, i32, "col_idx", _capacity(s)), _ptr(row_order, i32, "row_order", rows),
         _ptr(workspace, None, "workspace"), ctypes.c_size_t(ws_bytes), _stream(stream)),
         "wise_support_from_masks")
 
