@@ -279,8 +279,18 @@ struct WaveRows {
 constexpr int kMassChunk = 256;   // workspace entries reduced per epilogue pass
 constexpr int kMassBatch = 16;    // entry loads in flight per half-wave in the epilogue
 
+// Waves per SIMD the register allocator must leave room for.  Two by default
+// (the d-128 tiles hold 190-250 VGPRs).  The four-wave dense group at d 96
+// and the one-wave 32-key sparse group at d 96 fit in 168 VGPRs (three
+// waves), the 32-key sparse group at d 64 in 128 (four): more resident waves
+// hide more of each one's staging latency (2-6% on those kernels).
+constexpr int dense_waves_per_simd(int d, int nw) { return d == 96 && nw == 4 ? 3 : 2; }
+constexpr int sparse_waves_per_simd(int d, int kt) {
+  return kt != 32 ? 2 : d == 64 ? 4 : d == 96 ? 3 : 2;
+}
+
 template <int D, int NW, int BM>
-__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(dense_waves_per_simd(D, NW))))
 dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                   const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
                   float* __restrict__ lse, int n, int heads, int gq, Sched sc, float c,
@@ -290,8 +300,14 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   constexpr bool kMass = BM > 0;
   constexpr int kE = BM == 32 ? 32 : 64;            // keys per workspace entry
   constexpr int kEPT = kKeyTile / kE;               // entries per 64-key tile
-  __shared__ __attribute__((aligned(16))) uint16_t ks[G::kKElems];
-  __shared__ __attribute__((aligned(16))) uint16_t vt[G::kVElems];
+  // An 8-wave group fills its CU alone (two waves per SIMD), so no other
+  // group runs while it waits at a barrier: it keeps two LDS tiles and stages
+  // tile it+1 into the other one right after computing tile it, one barrier
+  // per tile.  Smaller groups share a CU three or four at a time, which a
+  // second buffer would halve; they stage and compute around two barriers.
+  constexpr int kBufs = NW == 8 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[kBufs * G::kKElems];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[kBufs * G::kVElems];
   int bh, item;
   if (!sched_slot(sc, bh, item)) return;
   const int qt = sc.items - 1 - item;
@@ -328,23 +344,56 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   const int nfull = qbase / kKeyTile;
   TileStage<D, kNT, true> st;
   st.load(rk, rv, 0, tid);
-  for (int it = 0; it < nfull; ++it) {
+  if constexpr (kBufs == 2) {
     st.store(ks, vt, tid);
+    if (ntiles > 1) st.load(rk, rv, kKeyTile, tid);
     __syncthreads();
-    st.load(rk, rv, (it + 1) * kKeyTile, tid);
-    w.template attend<false, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
-    put_mass(it);
-    __syncthreads();
-  }
-  for (int it = nfull; it < ntiles; ++it) {
-    st.store(ks, vt, tid);
-    __syncthreads();
-    if (it + 1 < ntiles) st.load(rk, rv, (it + 1) * kKeyTile, tid);
-    if (it * kKeyTile <= q0) {
-      w.template attend<true, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+    // Buffer (it+1)&1 was last read by tile it-1, which every wave finished
+    // before the previous barrier.
+    auto stage_next = [&](int it) {
+      if (it + 1 < ntiles) {
+        const int nx = (it + 1) & 1;
+        st.store(ks + nx * G::kKElems, vt + nx * G::kVElems, tid);
+        if (it + 2 < ntiles) st.load(rk, rv, (it + 2) * kKeyTile, tid);
+      }
+      __syncthreads();
+    };
+    int it = 0;
+    for (; it < nfull; ++it) {
+      const int cu = it & 1;
+      w.template attend<false, 2, kMass>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
+                                         it * kKeyTile, q0);
       put_mass(it);
+      stage_next(it);
     }
-    __syncthreads();
+    for (; it < ntiles; ++it) {
+      const int cu = it & 1;
+      if (it * kKeyTile <= q0) {
+        w.template attend<true, 2, kMass>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
+                                          it * kKeyTile, q0);
+        put_mass(it);
+      }
+      stage_next(it);
+    }
+  } else {
+    for (int it = 0; it < nfull; ++it) {
+      st.store(ks, vt, tid);
+      __syncthreads();
+      st.load(rk, rv, (it + 1) * kKeyTile, tid);
+      w.template attend<false, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+      put_mass(it);
+      __syncthreads();
+    }
+    for (int it = nfull; it < ntiles; ++it) {
+      st.store(ks, vt, tid);
+      __syncthreads();
+      if (it + 1 < ntiles) st.load(rk, rv, (it + 1) * kKeyTile, tid);
+      if (it * kKeyTile <= q0) {
+        w.template attend<true, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+        put_mass(it);
+      }
+      __syncthreads();
+    }
   }
   w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
   if constexpr (kMass) {
@@ -406,7 +455,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
 // stay in its L2.
 // ---------------------------------------------------------------------------
 template <int D, int NW, int KT>
-__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(sparse_waves_per_simd(D, KT))))
 sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
                    const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
