@@ -242,6 +242,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="4k")
+    ap.add_argument("--tau", type=float, default=None,
+                    help="selection threshold of the main workload (default: its first)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-regime", action="store_true")
     ap.add_argument("--no-paper-geometry", action="store_true",
@@ -269,7 +271,9 @@ def main():
         del src, dst
     cfg = CONFIGS[args.config]
     log(f"[bench] {cfg.name}: generating {cfg.steps} steps of inputs")
-    main_res = measure(cfg, args.steps, args.warmup, diag=not args.no_diagnostics)
+    if args.tau is not None and not 0.0 < args.tau <= 1.0:
+        ap.error("--tau must lie in (0, 1]")
+    main_res = measure(cfg, args.steps, args.warmup, tau=args.tau, diag=not args.no_diagnostics)
     log(f"[bench] {json.dumps(main_res)}")
     pr = pu = None
     if not args.no_paper_regime and args.config == "4k":
@@ -308,7 +312,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: batch {cfg.batch}, {cfg.heads} heads, d {cfg.head_dim}, "
                                f"seq {cfg.seq_len}, block {cfg.block}, {cfg.discovery_steps} discovery "
-                               f"+ {cfg.late_steps} late steps, tau {cfg.tau}, planted gain "
+                               f"+ {cfg.late_steps} late steps, tau {main_res['tau']}, planted gain "
                                f"{cfg.gain}",
                    "step": "one full trajectory (discovery + mass pooling, selection, late sparse)",
                    "density": round(main_res["density"], 4)},
@@ -317,7 +321,7 @@ def main():
                              ("speedup_prepared", "speedup_setup_inclusive", "speedup_trajectory")},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
-                     "traffic": measured_traffic(cfg.name),
+                     "traffic": measured_traffic(cfg.name) if args.tau is None else None,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                      "kernel": "sparse_attn_kernel",
                      "flops_per_launch": eff, "avg_launch_ms": round(main_res["late_ms_mean"], 5)},
