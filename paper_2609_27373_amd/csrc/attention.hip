@@ -475,7 +475,11 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qb * kB + 32 * wave;
   const int beg = row_ptr[row];
-  const int nent = row_ptr[row + 1] - beg;
+  int nent = row_ptr[row + 1] - beg;
+  // Ids past the diagonal form a suffix of the ascending row: dropping them
+  // leaves the diagonal block, when present, as the last entry, the one the
+  // masked tail below handles.
+  while (nent > 0 && col_idx[beg + nent - 1] > qb) --nent;
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
 

@@ -77,3 +77,65 @@ def test_explicit_kv_heads_equal_heads_is_plain_attention(gpu_lib):
     torch.cuda.synchronize()
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("gq,d", [(2, 64), (4, 96), (8, 128), (4, 64)])
+def test_shared_kv_heads_match_repeated_kv(gpu_lib, gq, d):
+    """32-key blocks, kv_heads < heads: every query head comes out bit for bit
+    as with its key-value head repeated explicitly (kv_heads = heads), and a
+    sampled head per batch matches the oracle.  Supports: random per query
+    head, with empty rows, local bands, ids past the diagonal after the
+    diagonal block, and 130 query blocks."""
+    w = gpu_lib
+    bt, kvh, n, B = 2, 2, 32 * 130, 32
+    h = gq * kvh
+    nb = n // B
+    say(f"shared kv heads gq={gq} d={d} heads={h} n={n}")
+    q, k, v = (x.cuda() for x in make(bt, h, kvh, n, d, seed=7 * gq + d))
+    rng = np.random.default_rng(gq * 1000 + d)
+    rp, ci = [0], []
+    for bh in range(bt * h):
+        for qb in range(nb):
+            u = rng.random()
+            if u < 0.05:
+                ids = []                                          # empty row
+            elif u < 0.15:
+                ids = sorted({0, qb} | set(range(max(0, qb - 5), qb)))   # local band
+            else:
+                ids = sorted(set(np.nonzero(rng.random(qb + 1) < 0.3)[0].tolist()) | {qb})
+                if u > 0.95:
+                    ids = ids + [qb + 1 + int(rng.integers(3))]    # past the diagonal
+            ci.extend(ids)
+            rp.append(len(ci))
+    rp_t = torch.tensor(rp, dtype=torch.int32, device="cuda")
+    ci_t = torch.tensor(ci, dtype=torch.int32, device="cuda")
+    s_g = w.make_shape(bt, h, n, d, B, kv_heads=kvh)
+    o_g = torch.empty_like(q)
+    l_g = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn(s_g, q, k, v, rp_t, ci_t, None, o_g, l_g)
+    ke = k.repeat_interleave(gq, dim=1).contiguous()
+    ve = v.repeat_interleave(gq, dim=1).contiguous()
+    s_r = w.make_shape(bt, h, n, d, B)
+    o_r = torch.empty_like(q)
+    l_r = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn(s_r, q, ke, ve, rp_t, ci_t, None, o_r, l_r)
+    torch.cuda.synchronize()
+    assert torch.equal(o_g, o_r)
+    assert torch.equal(l_g, l_r)
+    # and one sampled head per batch against the oracle
+    rows = np.array(rp, np.int32)
+    for bh in (0, h + gq):
+        b, hh = divmod(bh, h)
+        sl = slice(bh * nb, (bh + 1) * nb + 1)
+        rph = rows[sl] - rows[bh * nb]
+        cih = np.array(ci[rows[bh * nb]:rows[(bh + 1) * nb]], np.int32)
+        valid = np.concatenate([[x for x in cih[rph[i]:rph[i + 1]] if x <= i] for i in range(nb)]
+                               + [np.zeros(0)]).astype(np.int32)
+        cnt = [sum(1 for x in cih[rph[i]:rph[i + 1]] if x <= i) for i in range(nb)]
+        rpv = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int32)
+        qh = f64(q[b, hh])[None, None]
+        kh = f64(k[b, hh // gq])[None, None]
+        vh = f64(v[b, hh // gq])[None, None]
+        o_ref, l_ref = O.sparse_attention(qh, kh, vh, rpv, valid, B)
+        assert_attn(o_g[b, hh], o_ref[0, 0], f"head {bh} O")
+        assert_lse(l_g[b, hh], l_ref[0, 0], f"head {bh} lse")

@@ -47,7 +47,7 @@ def inputs(bt, h, n, d, seed, scale=1.0, planted=False):
     q = torch.randn((bt, h, n, d), generator=g) * scale
     k = torch.randn((bt, h, n, d), generator=g)
     v = torch.randn((bt, h, n, d), generator=g)
-    if planted:   # make some rows peaky so the lazy rescale path triggers
+    if planted:   # make some rows peaky so the O rescale path triggers
         q[..., ::7, :] *= 4
     return [x.to(torch.bfloat16) for x in (q, k, v)]
 
@@ -275,3 +275,29 @@ def test_determinism(gpu_lib):
                      s.col_idx[: s.nnz()].clone(), s.row_order.clone()))
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("B", [32, 64, 128])
+def test_sparse_ids_past_diagonal_after_the_diagonal(gpu_lib, B):
+    """Ids past the diagonal that follow the diagonal block are skipped and
+    the diagonal block is still attended (with its causal mask)."""
+    w = gpu_lib
+    bt, h, d = 1, 2, 64
+    nb = 4
+    n = nb * B
+    q, k, v = inputs(bt, h, n, d, seed=11 + B)
+    rows = [[0, 1], [0, 1, 2], [1, 2, 5], [3, 4, 7]]        # the (qb, id) pairs past qb are skipped
+    keep = [[x for x in r if x <= qb] for qb, r in enumerate(rows)]
+    rp = np.array([0] + list(np.cumsum([len(r) for r in rows * h])), np.int32)
+    ci = np.array([x for r in rows * h for x in r], np.int32)
+    rp_k = np.array([0] + list(np.cumsum([len(r) for r in keep * h])), np.int32)
+    ci_k = np.array([x for r in keep * h for x in r], np.int32)
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn(s, q.cuda(), k.cuda(), v.cuda(), torch.from_numpy(rp).cuda(),
+                       torch.from_numpy(ci).cuda(), None, o, lse)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp_k, ci_k, B)
+    assert_attn(o, o_ref, f"B{B} O")
+    assert_lse(lse, l_ref, f"B{B} lse")
