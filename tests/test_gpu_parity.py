@@ -56,6 +56,7 @@ SHAPES = [  # bt, h, n, d, B  (ragged: n not a multiple of 128, single block, ..
     (1, 1, 64, 64, 64), (2, 3, 384, 64, 64), (1, 2, 320, 96, 64), (1, 2, 640, 128, 64),
     (2, 2, 512, 128, 128), (1, 3, 384, 96, 128), (1, 1, 128, 64, 128), (1, 2, 1024, 128, 64),
     (1, 1, 64, 96, 32), (2, 2, 384, 96, 32), (1, 2, 320, 64, 32), (1, 3, 640, 128, 32),
+    (1, 2, 256, 128, 64), (1, 1, 768, 128, 32),   # one and three 256-query dense tiles
 ]
 
 
