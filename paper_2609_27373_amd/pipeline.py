@@ -92,3 +92,32 @@ class WisePipeline:
         wise.wise_sparse_attn(self.shape, q, k, v, s.row_ptr, s.col_idx,
                               s.row_order if ordered else None, out, lse)
         return out
+
+    def capture_late_step(self, q, k, v, out, lse=None) -> "LateStepGraph":
+        """The late step on these fixed buffers as a HIP graph (see LateStepGraph)."""
+        return LateStepGraph(self, q, k, v, out, lse)
+
+
+class LateStepGraph:
+    """One late step captured in a HIP graph over fixed q/k/v/out (and lse)
+    buffers.  A serving loop writes each step's Q/K/V into those buffers and
+    calls replay(): one launch of the recorded sparse kernel, which reads the
+    support held in the pipeline's schedule buffers at replay time (so a new
+    select() needs no re-capture).  The library allocates and clears nothing,
+    so the graph holds only the kernel node."""
+
+    def __init__(self, pipe: WisePipeline, q, k, v, out, lse=None):
+        self.buffers = (q, k, v, out, lse)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):              # warm-up launch outside the capture
+            pipe.late_step(q, k, v, out, lse)
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            pipe.late_step(q, k, v, out, lse)
+
+    def replay(self):
+        self.graph.replay()
+        return self.buffers[3]
+

@@ -91,3 +91,37 @@ def test_graph_replays_match_eager(gpu_lib):
         torch.cuda.synchronize()
         assert torch.equal(scratch, eager)
     assert torch.equal(pipe.acc, acc_eager)
+
+
+def test_captured_late_step_follows_new_inputs_and_supports(gpu_lib):
+    """LateStepGraph: replays after writing new Q/K/V into the captured
+    buffers, and after a new selection, give the eager late step's bits."""
+    cfg = CONFIGS["tiny"].with_(heads=4, seq_len=1024)
+    say(f"late-step graph: heads {cfg.heads} n {cfg.seq_len}")
+    steps = _trajectory_inputs(cfg, cfg.discovery_steps + 3)
+    pipe = WisePipeline.for_config(cfg)
+    out = torch.empty_like(steps[0][0])
+    pipe.reset()
+    for t in range(1, cfg.discovery_steps + 1):
+        pipe.discovery_step(*steps[t - 1], out, accumulate=t in cfg.window)
+    pipe.select()
+    qb, kb, vb = (torch.empty_like(x) for x in steps[0])
+    ob = torch.empty_like(out)
+    g = pipe.capture_late_step(qb, kb, vb, ob)
+    eager = torch.empty_like(out)
+    for rep, (q, k, v) in enumerate(steps[cfg.discovery_steps:]):
+        qb.copy_(q); kb.copy_(k); vb.copy_(v)
+        ob.zero_()
+        g.replay()
+        pipe.late_step(q, k, v, eager)
+        torch.cuda.synchronize()
+        assert torch.equal(ob, eager), f"replay {rep}"
+    # a different support (tau lowered): the graph reads the new CSR
+    pipe.tau = 0.5
+    pipe.select()
+    q, k, v = steps[-1]
+    qb.copy_(q); kb.copy_(k); vb.copy_(v)
+    g.replay()
+    pipe.late_step(q, k, v, eager)
+    torch.cuda.synchronize()
+    assert torch.equal(ob, eager), "replay after a new selection"
