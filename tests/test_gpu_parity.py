@@ -302,3 +302,38 @@ def test_sparse_ids_past_diagonal_after_the_diagonal(gpu_lib, B):
     o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp_k, ci_k, B)
     assert_attn(o, o_ref, f"B{B} O")
     assert_lse(lse, l_ref, f"B{B} lse")
+
+
+@pytest.mark.parametrize("d,B,scale", [(64, 64, 0.05), (128, 32, 0.2), (96, 128, 0.08)])
+def test_explicit_scale(gpu_lib, d, B, scale):
+    """wise_shape.scale > 0 replaces 1/sqrt(d) in dense attention, the pooled
+    masses and the late step alike."""
+    w = gpu_lib
+    bt, h, n = 1, 2, 512
+    say(f"explicit scale {scale} d={d} B={B}")
+    q, k, v = inputs(bt, h, n, d, seed=int(scale * 1000) + d, scale=2.0)
+    s = w.make_shape(bt, h, n, d, B, scale=scale)
+    nb = n // B
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    acc = torch.zeros((bt, h, nb, nb), device="cuda")
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    w.wise_dense_attn_accum(s, qd, kd, vd, o, lse, acc, w.mass_workspace(s))
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.dense_attention(f64(q), f64(k), f64(v), scale=scale)
+    assert_attn(o, o_ref, "scaled dense O")
+    assert_lse(lse, l_ref, "scaled dense lse")
+    assert np.abs(f64(acc) - O.block_mass(f64(q), f64(k), B, scale=scale)).max() <= ACC_TOL
+    rng = np.random.default_rng(d + B)
+    rp, ci = [0], []
+    for _ in range(bt * h):
+        for qb in range(nb):
+            ci.extend(sorted(set(rng.integers(0, qb + 1, size=2).tolist()) | {0, qb}))
+            rp.append(len(ci))
+    rp, ci = np.array(rp, np.int32), np.array(ci, np.int32)
+    w.wise_sparse_attn(s, qd, kd, vd, torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda(),
+                       None, o, lse)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp, ci, B, scale=scale)
+    assert_attn(o, o_ref, "scaled sparse O")
+    assert_lse(lse, l_ref, "scaled sparse lse")
