@@ -196,7 +196,7 @@ def test_select_only_parity(gpu_lib, nb, seed):
     s = w.make_shape(1, h, nb * 64, 64, 64)
     sched = w.Schedule(s)
     for tau in (0.5, 0.9, 0.95, 1.0):
-        for flags in (0, 1, 3):
+        for flags in (0, 1, 2, 3):
             t32 = float(np.float32(tau))
             sched.select(torch.from_numpy(acc).cuda(), t32, flags)
             torch.cuda.synchronize()
