@@ -255,12 +255,13 @@ def test_union_trajectory_tiny(gpu_lib):
     assert_attn(out, o_ref, "union late step")
 
 
-@pytest.mark.parametrize("name", ["4k-pr", "8k", "4k-b32"])
+@pytest.mark.parametrize("name", ["4k-pr", "8k", "4k-b32", "4k-gqa"])
 def test_union_fullsize(gpu_lib, name):
     """Full-size union mode: every CSR row well formed and the row order
-    valid, sampled rows of head 0 (per-step masses and the union) against the
-    oracle's own from the inputs, and the retained-mass diagnostic at that
-    size."""
+    valid, sampled rows of head 0 (and, with shared key-value heads, of the
+    last query head of the last batch, on another key-value head) against
+    the oracle's own per-step masses and union from the inputs, and the
+    retained-mass diagnostic at that size."""
     cfg = CONFIGS[name]
     say(f"union full-size {name}")
     tr = Trajectory(cfg, device="cuda")
@@ -269,6 +270,7 @@ def test_union_fullsize(gpu_lib, name):
     out = None
     gpu_r, kept = [], {}
     nb, B = cfg.nb, cfg.block
+    heads = [(0, 0)] + ([(cfg.batch - 1, cfg.heads - 1)] if cfg.grouped else [])
     for t in range(1, cfg.discovery_steps + 2):
         q, k, v = tr.next(torch.bfloat16)
         if out is None:
@@ -277,8 +279,9 @@ def test_union_fullsize(gpu_lib, name):
             pipe.discovery_step(q, k, v, out, accumulate=t in cfg.window)
             if t in cfg.window:
                 gpu_r.append(pipe.acc.cpu().numpy().copy())
-                kept[t] = (q[0, 0].float().cpu().double().numpy(),
-                           k[0, 0].float().cpu().double().numpy())
+                kept[t] = {(b, h): (q[b, h].float().cpu().double().numpy(),
+                                    k[b, O.kv_head(h, cfg.heads, cfg.kvh)].float().cpu().double()
+                                    .numpy()) for b, h in heads}
         else:
             pipe.select()
             frac, _ = diagnostics.retained_mass(pipe.shape, q, k, v, pipe.schedule)
@@ -288,21 +291,24 @@ def test_union_fullsize(gpu_lib, name):
     check_csr(rp, ci, nb, pipe.flags)
     check_row_order(pipe.schedule.row_order.cpu().numpy(), rp, nb)
     scale = 1.0 / np.sqrt(cfg.head_dim)
-    for qb in (0, nb // 2, nb - 1):
-        refs = []
-        for j, t in enumerate(cfg.window):
-            qh, kh = kept[t]
-            ref = O.block_mass_row(qh, kh, qb, B, scale)
-            assert np.abs(gpu_r[j][0, 0, qb] - ref).max() <= ACC_TOL
-            refs.append(ref)
-        want = set()
-        for ref in refs:
-            want.update(O.select_row(ref, qb, tau, flags=0))
-        want |= {0, qb}
-        got = [int(x) for x in ci[rp[qb]:rp[qb + 1]]]
-        if got != sorted(want):
-            assert any(near_tie(ref, qb, tau) for ref in refs), f"row {qb}: {got} vs {sorted(want)}"
-            say(f"  near-tie row {qb} reported")
+    for (b, h) in heads:
+        base = (b * cfg.heads + h) * nb
+        for qb in (0, nb // 2, nb - 1):
+            refs = []
+            for j, t in enumerate(cfg.window):
+                qh, kh = kept[t][(b, h)]
+                ref = O.block_mass_row(qh, kh, qb, B, scale)
+                assert np.abs(gpu_r[j][b, h, qb] - ref).max() <= ACC_TOL
+                refs.append(ref)
+            want = set()
+            for ref in refs:
+                want.update(O.select_row(ref, qb, tau, flags=0))
+            want |= {0, qb}
+            got = [int(x) for x in ci[rp[base + qb]:rp[base + qb + 1]]]
+            if got != sorted(want):
+                assert any(near_tie(ref, qb, tau) for ref in refs), \
+                    f"head ({b},{h}) row {qb}: {got} vs {sorted(want)}"
+                say(f"  near-tie row ({b},{h},{qb}) reported")
     dens = rp[-1] / (cfg.batch * cfg.heads * nb * (nb + 1) / 2)
     say(f"  union density {dens:.4f}, retained future mass (step t_d+1) {frac:.4f}")
     assert 0.0 < frac <= 1.0 + 1e-9 and frac >= 0.9 * cfg.tau
