@@ -20,9 +20,11 @@ sample as a baseline only.
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -58,6 +60,28 @@ def kernel_digest():
         with open(os.path.join(ROOT, "paper_2609_27373_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def device_clock():
+    """Compute units (torch) and the highest engine-clock level the driver
+    lists (sysfs pp_dpm_sclk, e.g. "1: 2400Mhz *"), with the bf16 MFMA peak
+    at that clock: four SIMDs per CU, each finishing a 32x32x16 bf16 MFMA
+    (32768 FLOP) every 32 cycles, so CUs x 4096 FLOP per clock.  The clock
+    fields are None where the driver does not list the levels."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    mhz = None
+    for f in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            levels = [int(m.group(1)) for m in
+                      (re.search(r"(\d+)\s*mhz", ln.lower()) for ln in open(f)) if m]
+        except OSError:
+            continue
+        if levels:
+            mhz = max(levels)
+            break
+    peak = cus * 4096 * mhz * 1e6 / 1e12 if mhz else None
+    return {"cus": cus, "sclk_max_mhz": mhz,
+            "bf16_peak_at_clock_tflops": round(peak, 1) if peak else None}
 
 
 def measured_traffic(name):
@@ -324,7 +348,8 @@ def main():
                      "traffic": measured_traffic(cfg.name) if args.tau is None else None,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                      "kernel": "sparse_attn_kernel",
-                     "flops_per_launch": eff, "avg_launch_ms": round(main_res["late_ms_mean"], 5)},
+                     "flops_per_launch": eff, "avg_launch_ms": round(main_res["late_ms_mean"], 5),
+                     "device": device_clock()},
         "cpu_baseline": cpu,
         "detail": {k: (round(v, 5) if isinstance(v, float) else v) for k, v in main_res.items()},
         "paper_regime": None if pr is None else {
