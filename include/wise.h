@@ -34,6 +34,9 @@
  *    synchronisation.  WISE_ERR_HIP carries a failed launch.
  *  - Calls are stateless and re-entrant; calls on different streams with
  *    disjoint outputs may run concurrently.  No C++ exception crosses the ABI.
+ *  - A successful call enqueues kernels only: no allocation, memset, copy or
+ *    synchronisation, so calls may be captured in a HIP graph (the graph
+ *    then reads whatever the captured buffers hold at replay time).
  *  - Supported: head_dim in {64, 96, 128}; block in {32, 64, 128};
  *    seq_len % block == 0, and seq_len % 64 == 0 for block 32 (the dense
  *    kernel's key tiles); nb <= 1024 for wise_select_support,
