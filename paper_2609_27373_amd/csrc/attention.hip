@@ -34,8 +34,9 @@ namespace wise {
 // 32-key blocks; K rows permuted so the S^T accumulator comes out in PV
 // operand order; V rows in natural order).  Loads for the next tile are
 // issued before the current one is computed, so the memory latency hides
-// behind the MFMA work; stores follow the barrier that retires the current
-// tile.
+// behind the MFMA work; stores go to an LDS tile no wave still reads: after
+// the barrier that retires it, or, in the 8-wave dense group, into its
+// second buffer.
 // ---------------------------------------------------------------------------
 template <int D, int NT, bool kWithV, int KT = kKeyTile>
 struct TileStage {
