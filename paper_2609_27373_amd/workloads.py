@@ -164,66 +164,62 @@ def _gen(device, seed: int, tag: int) -> torch.Generator:
     return g
 
 
+# Stream tags of the Gaussian draws.  Each draw covers a whole tensor (every
+# head at once), so a step costs three generator launches whatever the head
+# count; a head subset is the same draw sliced.
+_TAG_K0, _TAG_V0, _TAG_QNOISE = 1, 2, 3
+
+
+def _step_tag(t: int, which: int) -> int:
+    return (t << 4) | (4 + which)          # which: 0 = Q, 1 = K, 2 = V
+
+
+def _randn(shape, device, seed: int, tag: int) -> torch.Tensor:
+    return torch.randn(shape, generator=_gen(device, seed, tag), device=device)
+
+
+def _plant_weights(cfg: WorkloadConfig) -> torch.Tensor:
+    """[batch*heads][nb][nb] fp32: row q of head h averages the key tiles of
+    its planted blocks (weight 1/|rel| on each)."""
+    rel = relevant_blocks(cfg)
+    nb = cfg.nb
+    W = np.zeros((len(rel), nb, nb), dtype=np.float32)
+    for hid, per_q in enumerate(rel):
+        for q, r in enumerate(per_q):
+            W[hid, q, r] = 1.0 / len(r)
+    return torch.from_numpy(W)
+
+
 def planted_base(cfg: WorkloadConfig, device="cpu", heads: Optional[Sequence[int]] = None):
-    """fp32 (Q0, K0, V0), each [batch][heads][n][d], on `device`.
+    """fp32 (Q0, K0, V0) on `device`: Q0 [batch][heads][n][d], K0 and V0
+    [batch][kv_heads][n][d].
 
-    `heads` restricts generation to a subset of flattened (b*heads + h) ids
-    (the returned tensors are then [1][len(heads)][n][d]); each head's draws
-    depend only on (seed, head id), so a subset reproduces the full tensor's
-    slices exactly.
+    `heads` restricts the result to a subset of flattened (b*heads + h) ids
+    (the tensors are then [1][len(heads)][n][d]); the subset is a slice of the
+    full draw, so it matches the full tensor exactly.
     """
+    if heads is not None and cfg.grouped:
+        raise ValueError("head subsets are not drawn for grouped-query workloads")
+    n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
+    bh, bkv = cfg.batch * cfg.heads, cfg.batch * cfg.kvh
+    K = _randn((bkv, n, d), device, cfg.seed, _TAG_K0)
+    V = _randn((bkv, n, d), device, cfg.seed, _TAG_V0)
+    noise = _randn((bh, nb, B * d), device, cfg.seed, _TAG_QNOISE)
     if cfg.grouped:
-        if heads is not None:
-            raise ValueError("head subsets are not drawn for grouped-query workloads")
-        return _planted_grouped(cfg, device)
-    n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
-    rel = relevant_blocks(cfg)
-    ids = list(range(cfg.batch * cfg.heads)) if heads is None else list(heads)
-    Q = torch.empty((len(ids), n, d), dtype=torch.float32, device=device)
-    K = torch.empty_like(Q)
-    V = torch.empty_like(Q)
-    for slot, hid in enumerate(ids):
-        g = _gen(device, cfg.seed, 1 + hid)
-        K[slot] = torch.randn((n, d), generator=g, device=device)
-        V[slot] = torch.randn((n, d), generator=g, device=device)
-        W = torch.zeros((nb, nb), dtype=torch.float32)
-        for q, r in enumerate(rel[hid]):
-            W[q, torch.as_tensor(r)] = 1.0 / len(r)
-        W = W.to(device)
-        mean_tiles = W @ K[slot].reshape(nb, B * d)
-        noise = torch.randn((nb, B * d), generator=g, device=device)
-        Q[slot] = (cfg.gain * mean_tiles + cfg.noise * noise).reshape(n, d)
-    if heads is None:
-        shape = (cfg.batch, cfg.heads, n, d)
+        G = cfg.heads // cfg.kvh
+        kid = torch.tensor([(h // cfg.heads) * cfg.kvh + (h % cfg.heads) // G for h in range(bh)],
+                           device=device)
+        Kq = K.index_select(0, kid)
     else:
+        Kq = K
+    mean_tiles = torch.bmm(_plant_weights(cfg).to(device), Kq.reshape(bh, nb, B * d).contiguous())
+    Q = (cfg.gain * mean_tiles + cfg.noise * noise).reshape(bh, n, d)
+    del noise, mean_tiles, Kq
+    if heads is not None:
+        ids = torch.tensor(list(heads), device=device)
         shape = (1, len(ids), n, d)
-    return Q.reshape(shape), K.reshape(shape), V.reshape(shape)
-
-
-_KV_TAG = 1 << 20   # stream ids of key-value heads, apart from query heads
-
-
-def _planted_grouped(cfg: WorkloadConfig, device):
-    n, d, B, nb = cfg.seq_len, cfg.head_dim, cfg.block, cfg.nb
-    G = cfg.heads // cfg.kvh
-    rel = relevant_blocks(cfg)
-    K = torch.empty((cfg.batch * cfg.kvh, n, d), dtype=torch.float32, device=device)
-    V = torch.empty_like(K)
-    for kid in range(cfg.batch * cfg.kvh):
-        g = _gen(device, cfg.seed, _KV_TAG + kid)
-        K[kid] = torch.randn((n, d), generator=g, device=device)
-        V[kid] = torch.randn((n, d), generator=g, device=device)
-    Q = torch.empty((cfg.batch * cfg.heads, n, d), dtype=torch.float32, device=device)
-    for hid in range(cfg.batch * cfg.heads):
-        b, h = divmod(hid, cfg.heads)
-        kid = b * cfg.kvh + h // G
-        g = _gen(device, cfg.seed, 1 + hid)
-        W = torch.zeros((nb, nb), dtype=torch.float32)
-        for q, r in enumerate(rel[hid]):
-            W[q, torch.as_tensor(r)] = 1.0 / len(r)
-        mean_tiles = W.to(device) @ K[kid].reshape(nb, B * d)
-        noise = torch.randn((nb, B * d), generator=g, device=device)
-        Q[hid] = (cfg.gain * mean_tiles + cfg.noise * noise).reshape(n, d)
+        return (Q.index_select(0, ids).reshape(shape), K.index_select(0, ids).reshape(shape),
+                V.index_select(0, ids).reshape(shape))
     return (Q.reshape(cfg.batch, cfg.heads, n, d), K.reshape(cfg.batch, cfg.kvh, n, d),
             V.reshape(cfg.batch, cfg.kvh, n, d))
 
@@ -234,42 +230,29 @@ class Trajectory:
     Step t (1-based) holds X_t = X_{t-1} + eps_t for X in {Q, K, V}, with
     X_0 the planted base.  `next()` returns the step's tensors in the
     working dtype (bf16, round-to-nearest-even, unless cfg.dtype is fp32)
-    and advances; the fp32 random-walk state stays on `device`.  The step
-    noise of each head is drawn from its own (seed, head, step) stream, so a
-    head subset reproduces the full trajectory's slices on the same device.
+    and advances; the fp32 random-walk state stays on `device`.  Each
+    tensor's step noise is one draw over all its heads from the (seed, step,
+    tensor) stream; a head subset takes its slice of that draw, so it
+    reproduces the full trajectory's slices on the same device.
     """
 
     def __init__(self, cfg: WorkloadConfig, device="cpu", heads=None):
         self.cfg = cfg
         self.device = device
-        self.ids = list(range(cfg.batch * cfg.heads)) if heads is None else list(heads)
+        self.ids = None if heads is None else torch.tensor(list(heads), device=device)
         self.state = list(planted_base(cfg, device, heads))
         self.t = 0
 
     def next(self, dtype=None):
         self.t += 1
-        n, d = self.cfg.seq_len, self.cfg.head_dim
-        if self.cfg.grouped:
-            self._step_grouped()
-            dt = dtype or (torch.float32 if self.cfg.dtype == "fp32" else torch.bfloat16)
-            return tuple(x.to(dt).contiguous() for x in self.state)
-        for slot, hid in enumerate(self.ids):
-            g = _gen(self.device, self.cfg.seed, (1 + hid) * 65536 + self.t)
-            for x in self.state:
-                flat = x.view(-1, n, d)
-                flat[slot].add_(torch.randn((n, d), generator=g, device=self.device),
-                                alpha=self.cfg.step_noise)
-        dt = dtype or (torch.float32 if self.cfg.dtype == "fp32" else torch.bfloat16)
+        c = self.cfg
+        n, d = c.seq_len, c.head_dim
+        full = (c.batch * c.heads, c.batch * c.kvh, c.batch * c.kvh)
+        for which, x in enumerate(self.state):
+            eps = _randn((full[which], n, d), self.device, c.seed, _step_tag(self.t, which))
+            if self.ids is not None:
+                eps = eps.index_select(0, self.ids)
+            x.view(-1, n, d).add_(eps, alpha=c.step_noise)
+            del eps
+        dt = dtype or (torch.float32 if c.dtype == "fp32" else torch.bfloat16)
         return tuple(x.to(dt).contiguous() for x in self.state)
-
-    def _step_grouped(self):
-        n, d, c = self.cfg.seq_len, self.cfg.head_dim, self.cfg
-        q, k, v = (x.view(-1, n, d) for x in self.state)
-        for hid in range(c.batch * c.heads):
-            g = _gen(self.device, c.seed, (1 + hid) * 65536 + self.t)
-            q[hid].add_(torch.randn((n, d), generator=g, device=self.device), alpha=c.step_noise)
-        for kid in range(c.batch * c.kvh):
-            g = _gen(self.device, c.seed, (_KV_TAG + kid) * 65536 + self.t)
-            for x in (k, v):
-                x[kid].add_(torch.randn((n, d), generator=g, device=self.device),
-                            alpha=c.step_noise)

@@ -6,6 +6,11 @@ import torch
 from oracle import wise_oracle as O
 
 ATOL_MAX, ATOL_MEAN, LSE_TOL, ACC_TOL, TIE = 1e-2, 1e-3, 1e-3, 1e-5, 1e-5
+# Outputs are bf16: rounding alone costs up to half a spacing, 2^-8 |x| at
+# most, i.e. up to 0.0078 for |x| in [2, 4), which leaves the 1e-2 max-abs bar
+# almost no room for the kernel.  The bar applies where |ref| < BIG; beyond,
+# the error must stay within one bf16 spacing (2^-7 |ref|).
+BIG = 2.0
 
 
 def f64(t):
@@ -19,16 +24,29 @@ def say(*a):
 def attn_errors(gpu, ref):
     g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
     err = np.abs(g - ref)
-    big = np.abs(ref) >= 4.0
+    big = np.abs(ref) >= BIG
     small_max = err[~big].max() if (~big).any() else 0.0
     big_ratio = (err[big] / (2.0 ** -7 * np.abs(ref[big]))).max() if big.any() else 0.0
     return err, small_max, big_ratio, int(big.sum())
 
 
+def bf16_round(x):
+    """float64 -> nearest bf16 value (ties to even), back in float64."""
+    return torch.from_numpy(np.asarray(x, dtype=np.float64)).to(torch.bfloat16).double().numpy()
+
+
 def assert_attn(gpu, ref, what=""):
+    """Bars on |gpu - ref|; the report also splits the error into the part
+    bf16 output rounding alone costs (|bf16(ref) - ref|) and the kernel's own
+    part (|gpu - bf16(ref)|)."""
     err, small_max, big_ratio, nbig = attn_errors(gpu, ref)
-    say(f"  {what}: max-abs {err.max():.3g} (|ref|<4: {small_max:.3g}; {nbig} outputs |ref|>=4 "
-        f"at {big_ratio:.2f} spacing) mean-abs {err.mean():.3g}")
+    g = f64(gpu) if isinstance(gpu, torch.Tensor) else gpu
+    rr = bf16_round(ref)
+    fmt, ker = np.abs(rr - ref), np.abs(g - rr)
+    say(f"  {what}: max-abs {err.max():.3g} (|ref|<{BIG:g}: {small_max:.3g}; {nbig} outputs |ref|>={BIG:g} "
+        f"at {big_ratio:.2f} spacing) mean-abs {err.mean():.3g} | bf16 rounding of ref: max "
+        f"{fmt.max():.3g} mean {fmt.mean():.3g} | kernel vs bf16(ref): max {ker.max():.3g} "
+        f"mean {ker.mean():.3g}")
     assert small_max <= ATOL_MAX and big_ratio <= 1.0 and err.mean() <= ATOL_MEAN, \
         f"{what}: max {err.max():.3g} (small {small_max:.3g}, big {big_ratio:.2f}) mean {err.mean():.3g}"
 
@@ -53,6 +71,52 @@ def near_tie(v, qb, tau):
     return min(m["delta_minus"], m["delta_plus"], m["delta_rank"]) < TIE
 
 
+def tie_alternatives(v, qb, tau, flags):
+    """The supports a cut within TIE of a boundary admits, from the oracle's
+    own masses v[0..qb] (normalised by the row total): one block fewer when
+    delta^- < TIE, one more when delta^+ < TIE, and any kept block swapped
+    for a dropped one whose normalised mass is within 2 TIE of it (delta^rank
+    is the adjacent case).  Forced blocks are added to each.  Empty when the
+    cut is not near a boundary."""
+    v = np.asarray(v, dtype=np.float64)[: qb + 1]
+    total = v.sum()
+    if total <= 0:
+        return []
+    w = v / total
+    m = O.support_margins(v, qb, tau)
+    k = m["kstar"]
+    order = [int(b) for b in np.lexsort((np.arange(qb + 1), -w))]
+    forced = set()
+    if flags & 1:
+        forced.add(0)
+    if flags & 2:
+        forced.add(qb)
+    out = []
+    if m["delta_minus"] < TIE and k >= 1:
+        out.append(set(order[:k - 1]))
+    if m["delta_plus"] < TIE and k < qb + 1:
+        out.append(set(order[:k + 1]))
+    kept, dropped = order[:k], order[k:]
+    for a in kept:
+        for b in dropped:
+            if abs(w[a] - w[b]) < 2 * TIE:
+                out.append((set(kept) - {a}) | {b})
+    return [sorted((s | forced) or {qb}) for s in out]
+
+
+def check_row_vs_oracle(got, v, qb, tau, flags, what):
+    """An end-to-end CSR row against the oracle's selection on its own
+    masses v.  Returns True when equal, False for a reported near tie (the
+    GPU row is one of the alternatives the tie admits); fails otherwise."""
+    want = O.select_row(v, qb, tau, flags)
+    got = [int(x) for x in got]
+    if got == want:
+        return True
+    alts = tie_alternatives(v, qb, tau, flags)
+    assert got in alts, f"{what}: gpu {got} oracle {want} (no near tie admits it)"
+    return False
+
+
 def compare_support(gpu_rows, acc_ref, tau, flags, row_ids=None):
     """End-to-end CSR rows vs the oracle's selection on its own accumulator."""
     bt, h, nb, _ = acc_ref.shape
@@ -60,17 +124,35 @@ def compare_support(gpu_rows, acc_ref, tau, flags, row_ids=None):
     reported = []
     ids = range(bt * h * nb) if row_ids is None else row_ids
     for i, r in enumerate(ids):
-        qb = r % nb
-        want = O.select_row(flat[r], qb, tau, flags)
-        got = [int(x) for x in gpu_rows[i]]
-        if got != want:
-            assert near_tie(flat[r], qb, tau), f"row {r}: gpu {got} oracle {want}"
+        if not check_row_vs_oracle(gpu_rows[i], flat[r], r % nb, tau, flags, f"row {r}"):
             reported.append(r)
     if reported:
         say(f"near-tie CSR rows reported (not failed): {reported[:20]} ({len(reported)})")
     return reported
 
 
+def synthetic_masses(rows_shape, seed, total=4.0):
+    """Host-generated fp32 block masses for selection-only checks: [..][nb][nb]
+    with every row qb filled on kb <= qb (zero above), heavy-tailed values,
+    exact ties planted in some rows, and some all-zero and one-block rows;
+    each row sums to about `total` (the window length)."""
+    *lead, nb, _ = rows_shape
+    R = int(np.prod(lead)) * nb
+    rng = np.random.default_rng(seed)
+    x = rng.exponential(size=(R, nb)) ** rng.uniform(1.0, 4.0, size=(R, 1))
+    qb = np.arange(R) % nb
+    x[np.arange(nb)[None, :] > qb[:, None]] = 0.0
+    ties = rng.random(R) < 0.15                       # copy one entry onto another
+    src = (rng.random(R) * (qb + 1)).astype(int)
+    dst = (rng.random(R) * (qb + 1)).astype(int)
+    x[ties, dst[ties]] = x[ties, src[ties]]
+    one = rng.random(R) < 0.02                         # a single non-zero block
+    x[one] = 0.0
+    x[one, src[one]] = 1.0
+    x[rng.random(R) < 0.02] = 0.0                      # rows never written
+    s = x.sum(1, keepdims=True)
+    x = np.where(s > 0, x * (total / np.where(s > 0, s, 1.0)), 0.0)
+    return x.astype(np.float32).reshape(rows_shape)
 
 
 def check_csr(rp, ci, nb, flags):
