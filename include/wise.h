@@ -17,7 +17,8 @@
  *  - Every tensor argument is a DEVICE pointer owned by the caller,
  *    contiguous, row-major.  The library allocates nothing: scratch space
  *    comes in as caller-owned workspaces sized by the *_workspace_bytes
- *    queries.
+ *    queries, except for wise_select_support_noalloc, which uses a fixed
+ *    device array of its own (WISE_NOALLOC_SCRATCH_BYTES per GPU).
  *  - bf16 tensors are raw IEEE bfloat16 storage (uint16, round-to-nearest-even
  *    when produced by the library).
  *  - Shapes: q, o are [batch][heads][seq_len][head_dim]; k, v are
@@ -60,7 +61,7 @@
 extern "C" {
 #endif
 
-#define WISE_ABI_VERSION 2
+#define WISE_ABI_VERSION 3
 
 typedef enum {
   WISE_OK = 0,
@@ -169,6 +170,37 @@ wise_status wise_select_support(const wise_shape* s, const float* acc,
                                 int32_t* col_idx, int32_t* row_order,
                                 void* workspace, size_t workspace_bytes,
                                 void* hip_stream);
+
+/* Bytes of the library's own per-device selection scratch (see
+ * wise_select_support_noalloc). */
+#define WISE_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+
+/*
+ * wise_select_support_noalloc — wise_select_support without a caller
+ * workspace, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same selection, CSR, row order, arguments and errors as
+ * wise_select_support, minus the workspace.  The per-row counts and
+ * bitmasks live instead in a device array of WISE_NOALLOC_SCRATCH_BYTES
+ * inside the library: every GPU the library runs on holds its own copy
+ * until the process ends, and its address is looked up on the first call on
+ * each device (the current device at the call).  The call performs no
+ * allocation, free, memset or copy: it only enqueues the selection kernels.
+ * Every row's scratch entries are written before they are read, so the
+ * array's contents from earlier calls do not matter; but all calls on one
+ * GPU share the array, so calls that overlap on one GPU (different streams
+ * without ordering, different host threads) race and must not be issued.
+ * Limit: wise_select_workspace_bytes(s) <= WISE_NOALLOC_SCRATCH_BYTES
+ * (4 MiB: e.g. 28,160 rows of 128 blocks need 0.56 MiB), else
+ * WISE_ERR_WORKSPACE and nothing is launched.
+ * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_RANGE,
+ *         WISE_ERR_WORKSPACE, WISE_ERR_HIP (also a failed address lookup).
+ */
+wise_status wise_select_support_noalloc(const wise_shape* s, const float* acc,
+                                        float tau, uint32_t flags,
+                                        int32_t* row_ptr, int32_t* col_idx,
+                                        int32_t* row_order, void* hip_stream);
 
 /*
  * wise_sparse_attn — attention of one late recurrent step restricted to a

@@ -26,6 +26,9 @@
 // "Stability of the Deployed Working Set") and the attention mass a support
 // retains from one step's block masses (Section 7.1 and Appendix B, the
 // retained future full-attention mass).
+#include <mutex>
+
+#include "wise.h"
 #include "wise_device.hpp"
 #include "wise_kernels.hpp"
 
@@ -273,6 +276,49 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
   launch_rows(s, acc, tau, flags, counts, masks, st);
   launch_csr(s, counts, masks, row_ptr, col_idx, row_order, st);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Selection with no caller workspace (wise_select_support_noalloc): the
+// per-row counts and bitmasks live in `scratch`, a file-scope device array of
+// WISE_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory, so kernels only ever receive the address the runtime
+// reports for the current device, looked up once per device.  Every row's
+// count and mask words are written before they are read, so nothing in the
+// array needs clearing; calls that overlap on one device share it and race.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[WISE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex scratch_mutex;
+static void* scratch_addr[kMaxDevices];
+
+static hipError_t device_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    scratch_addr[dev] = p;
+  }
+  *out = scratch_addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_select_noalloc(const Dims& s, const float* acc, float tau, uint32_t flags,
+                                 int32_t* row_ptr, int32_t* col_idx, int32_t* row_order,
+                                 hipStream_t st) {
+  if (select_workspace_bytes(s) > (size_t)WISE_NOALLOC_SCRATCH_BYTES) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = device_scratch(&ws);
+  if (e != hipSuccess) return e;
+  return launch_select(s, acc, tau, flags, row_ptr, col_idx, row_order, ws, st);
 }
 
 // ---------------------------------------------------------------------------

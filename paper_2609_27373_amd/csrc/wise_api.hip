@@ -90,6 +90,24 @@ wise_status wise_select_support(const wise_shape* s, const float* acc, float tau
                                       (hipStream_t)hip_stream));
 }
 
+wise_status wise_select_support_noalloc(const wise_shape* s, const float* acc, float tau,
+                                        uint32_t flags, int32_t* row_ptr, int32_t* col_idx,
+                                        int32_t* row_order, void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if (!acc || !row_ptr || !col_idx) return WISE_ERR_NULL;
+  if (d.nb > wise::kMaxSelectBlocks) return WISE_ERR_UNSUPPORTED;
+  if (!(tau > 0.f && tau <= 1.f)) return WISE_ERR_RANGE;
+  if (flags & ~(uint32_t)(WISE_FORCE_SINK | WISE_FORCE_DIAG)) return WISE_ERR_RANGE;
+  if (wise::select_workspace_bytes(d) > (size_t)WISE_NOALLOC_SCRATCH_BYTES) return WISE_ERR_WORKSPACE;
+  if (!aligned(acc, 4) || !aligned(row_ptr, 4) || !aligned(col_idx, 4) ||
+      (row_order && !aligned(row_order, 4)))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_select_noalloc(d, acc, tau, flags, row_ptr, col_idx, row_order,
+                                              (hipStream_t)hip_stream));
+}
+
 wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k, const void* v,
                              const int32_t* row_ptr, const int32_t* col_idx,
                              const int32_t* row_order, void* o, float* lse, void* hip_stream) {

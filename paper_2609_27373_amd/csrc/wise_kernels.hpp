@@ -28,6 +28,9 @@ hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t fl
                          int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, void* ws,
                          hipStream_t st);
 size_t select_workspace_bytes(const Dims& s);
+hipError_t launch_select_noalloc(const Dims& s, const float* acc, float tau, uint32_t flags,
+                                 int32_t* row_ptr, int32_t* col_idx, int32_t* row_order,
+                                 hipStream_t st);
 int mask_words(const Dims& s);
 hipError_t launch_select_step(const Dims& s, const float* r, float tau, uint64_t* mask,
                               hipStream_t st);

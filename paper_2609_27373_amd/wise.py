@@ -21,12 +21,14 @@ LIB_PATH = os.path.join(_PKG, "libwise.so")
 WISE_FORCE_SINK = 1
 WISE_FORCE_DIAG = 2
 WISE_DEFAULT_FLAGS = WISE_FORCE_SINK | WISE_FORCE_DIAG
+NOALLOC_SCRATCH_BYTES = 4 << 20    # WISE_NOALLOC_SCRATCH_BYTES
 
 STATUS_NAMES = {0: "WISE_OK", 1: "WISE_ERR_NULL", 2: "WISE_ERR_SHAPE", 3: "WISE_ERR_UNSUPPORTED",
                 4: "WISE_ERR_RANGE", 5: "WISE_ERR_WORKSPACE", 6: "WISE_ERR_HIP"}
 
 # Every symbol include/wise.h declares.
-EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_sparse_attn",
+EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_select_support_noalloc",
+           "wise_sparse_attn",
            "wise_select_step", "wise_support_from_masks", "wise_mask_union", "wise_mask_overlap",
            "wise_support_mass", "wise_mass_workspace_bytes", "wise_mask_words",
            "wise_select_workspace_bytes",
@@ -77,6 +79,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wise_select_support.argtypes = [S, P, ctypes.c_float, ctypes.c_uint32, P, P, P, P,
                                         ctypes.c_size_t, P]
     lib.wise_select_support.restype = ctypes.c_int
+    lib.wise_select_support_noalloc.argtypes = [S, P, ctypes.c_float, ctypes.c_uint32, P, P, P, P]
+    lib.wise_select_support_noalloc.restype = ctypes.c_int
     lib.wise_sparse_attn.argtypes = [S, P, P, P, P, P, P, P, P, P]
     lib.wise_sparse_attn.restype = ctypes.c_int
     lib.wise_select_step.argtypes = [S, P, ctypes.c_float, P, P]
@@ -182,6 +186,18 @@ def wise_select_support(s: wise_shape, acc, tau: float, flags: int, row_ptr, col
         _ptr(col_idx, i32, "col_idx", _capacity(s)), _ptr(row_order, i32, "row_order", rows),
         _ptr(workspace, None, "workspace"), ctypes.c_size_t(ws_bytes), _stream(stream)),
         "wise_select_support")
+
+
+def wise_select_support_noalloc(s: wise_shape, acc, tau: float, flags: int, row_ptr, col_idx,
+                                row_order=None, stream=None) -> None:
+    """wise_select_support on the library's own per-device scratch (no workspace)."""
+    _, _, nacc, rows = _sizes(s)
+    i32 = torch.int32
+    _check(_lib().wise_select_support_noalloc(
+        ctypes.byref(s), _ptr(acc, torch.float32, "acc", nacc), ctypes.c_float(tau),
+        ctypes.c_uint32(flags), _ptr(row_ptr, i32, "row_ptr", rows + 1),
+        _ptr(col_idx, i32, "col_idx", _capacity(s)), _ptr(row_order, i32, "row_order", rows),
+        _stream(stream)), "wise_select_support_noalloc")
 
 
 def wise_sparse_attn(s: wise_shape, q, k, v, row_ptr, col_idx, row_order, o, lse=None,

@@ -43,7 +43,7 @@ def test_exports(lib):
 
 
 def test_version_and_strings(lib):
-    assert wise.wise_abi_version() == 2
+    assert wise.wise_abi_version() == 3
     for st, name in wise.STATUS_NAMES.items():
         assert wise.wise_status_string(st).startswith(name)
     assert "unknown" in wise.wise_status_string(99)
@@ -178,3 +178,21 @@ def test_mask_and_mass_validation(lib, fn, args, status):
     assert getattr(lib, fn)(sh(S()), *args, None) == status
     assert getattr(lib, fn)(None, *args, None) == 1
     assert getattr(lib, fn)(sh(S(head_dim=80)), *args, None) == 3
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(s=None), 1), (dict(acc=None), 1), (dict(rp=None), 1), (dict(ci=None), 1),
+    (dict(tau=0.0), 4), (dict(tau=1.5), 4), (dict(flags=4), 4), (dict(s=S(block=96)), 3),
+    (dict(s=S(seq_len=64 * 2048)), 3), (dict(rp=MIS8.value + 1), 2),
+    # 1024 x 1024 rows of 1024 blocks need 132 MiB of scratch, past the 4 MiB array
+    (dict(s=S(batch=16, heads=64, seq_len=32 * 1024, block=32)), 5),
+])
+def test_select_noalloc_validation(lib, case, status):
+    s = case.pop("s", S())
+    a = dict(acc=FAKE, tau=0.9, flags=3, rp=FAKE, ci=FAKE)
+    a.update(case)
+    rp = ctypes.c_void_p(a["rp"]) if isinstance(a["rp"], int) else a["rp"]
+    assert lib.wise_select_support_noalloc(sh(s), a["acc"], ctypes.c_float(a["tau"]), a["flags"],
+                                           rp, a["ci"], None, None) == status
+    if s is not None and status == 5:
+        assert wise.wise_select_workspace_bytes(s) > wise.NOALLOC_SCRATCH_BYTES
