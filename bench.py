@@ -11,8 +11,13 @@ Reported `value`: effective TFLOP/s of the late-step sparse attention (4*d
 FLOPs per admitted causal (query, key) pair of the selected support), with
 its fraction of the bf16 dense MFMA peak, the speedup over this library's own
 dense kernel on the same late-step inputs, and the paper-regime variant of
-the same workload beside it.  The oracle (CPU, fp64) is timed on a bounded
-sample as a baseline only.
+the same workload beside it.  Further legs, each with its own manifest
+(seed, SHA-256 of the first and last step's inputs and of the CSR): the
+paper's geometry (4K, 220 heads, d 96, 32-key blocks) under both selection
+rules, with the same sparse kernel on the full causal support beside the
+selected one (the paper's matched-backend comparison); grouped-query
+attention; and the 8K, 16K (threshold sweep) and 32K workloads.  The oracle
+(CPU, fp64) is timed on a bounded sample as a baseline only.
 
     python bench.py [--steps K] [--warmup W] [--config 4k] [--gpus 1]
 """
@@ -97,6 +102,46 @@ def make_inputs(cfg):
     return steps
 
 
+def tensor_sha256(t):
+    """SHA-256 of a tensor's raw bytes (bf16 read as int16), host-side."""
+    x = t.detach()
+    if x.dtype == torch.bfloat16:
+        x = x.view(torch.int16)
+    return hashlib.sha256(x.contiguous().cpu().numpy().tobytes()).hexdigest()
+
+
+def manifest(cfg, steps, sched, tau, mode):
+    """Deterministic record of one leg: the generator's seed and parameters,
+    SHA-256 of the first and last step's Q/K/V, and of the selected CSR and
+    row order (rerunning with the same seed must reproduce every digest)."""
+    rp = sched.row_ptr
+    nnz = int(rp[-1].item())
+    csr = hashlib.sha256()
+    for t in (rp, sched.col_idx[:nnz], sched.row_order):
+        csr.update(t.view(torch.int32).cpu().numpy().tobytes())
+    return {
+        "seed": cfg.seed, "gain": cfg.gain, "relevant": list(cfg.relevant), "sink": cfg.sink,
+        "zipf": cfg.zipf, "noise": cfg.noise, "step_noise": cfg.step_noise, "tau": tau,
+        "rule": mode, "steps": cfg.steps,
+        "inputs_sha256": {f"step{t}_{n}": tensor_sha256(x)
+                          for t in (1, cfg.steps) for n, x in zip("qkv", steps[t - 1])},
+        "csr_sha256": csr.hexdigest(), "nnz": nnz,
+    }
+
+
+def full_support(cfg, device="cuda"):
+    """CSR of every causally admissible block (kb <= qb for every row):
+    the same sparse kernel on it is the matched full-support baseline."""
+    nb, rows = cfg.nb, cfg.batch * cfg.heads * cfg.nb
+    per_row = np.arange(1, nb + 1, dtype=np.int64)
+    counts = np.tile(per_row, rows // nb)
+    rp = np.zeros(rows + 1, np.int64)
+    rp[1:] = np.cumsum(counts)
+    ci = np.concatenate([np.arange(q + 1) for q in range(nb)]).astype(np.int32)
+    ci = np.tile(ci, rows // nb)
+    return (torch.from_numpy(rp.astype(np.int32)).to(device), torch.from_numpy(ci).to(device))
+
+
 class Timer:
     def __init__(self):
         self.pairs = []
@@ -165,8 +210,19 @@ def diagnose(cfg, pipe, steps):
             "j_td_T": st["j_td_T"]}
 
 
-def measure(cfg, K, W, tau=None, mode="accumulate", diag=False):
-    steps = make_inputs(cfg)
+def late_on_support(cfg, pipe, steps, out, rp, ci, timer, key):
+    """The late steps on an explicit CSR (natural longest-first row order)."""
+    for t in range(cfg.discovery_steps + 1, cfg.steps + 1):
+        q, k, v = steps[t - 1]
+        e = timer.start()
+        wise.wise_sparse_attn(pipe.shape, q, k, v, rp, ci, None, out)
+        timer.stop(e, key)
+
+
+def measure(cfg, K, W, tau=None, mode="accumulate", diag=False, steps=None, matched=False):
+    own = steps is None
+    if own:
+        steps = make_inputs(cfg)
     pipe = WisePipeline.for_config(cfg, tau=tau, mode=mode)
     out = torch.empty_like(steps[0][0])
     for _ in range(W):
@@ -199,10 +255,15 @@ def measure(cfg, K, W, tau=None, mode="accumulate", diag=False):
     late_ms, dense_ms, sel_ms = float(np.median(late)), float(np.median(dense)), float(np.median(sel))
     res = dict(
         workload=cfg.name, mode=mode, tau=float(tau if tau is not None else cfg.tau),
+        shape=f"batch {cfg.batch}, {cfg.heads} heads" + (f" over {cfg.kvh} kv heads" if cfg.grouped else "")
+              + f", d {cfg.head_dim}, seq {cfg.seq_len}, block {cfg.block}, {cfg.discovery_steps} discovery "
+              f"+ {cfg.late_steps} late steps",
+        timed_trajectories=K, warmup_trajectories=W,
         density=metrics.density(rp, cfg.nb, bh), nnz=int(rp[-1]),
         late_ms=late_ms, late_ms_mean=float(late.mean()),
         late_ms_iqr=[float(np.percentile(late, 25)), float(np.percentile(late, 75))],
         late_tflops=eff / (late.mean() * 1e-3) / 1e12,
+        pct_bf16_peak=100 * eff / (late.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         eff_flops_per_late_step=eff,
         dense_ms=dense_ms, dense_tflops=dflops / (dense.mean() * 1e-3) / 1e12,
         select_ms=sel_ms, discovery_ms=float(np.median(disc)),
@@ -210,11 +271,27 @@ def measure(cfg, K, W, tau=None, mode="accumulate", diag=False):
         speedup_setup_inclusive=(L * dense_ms) / (sel_ms + L * late_ms),
         speedup_trajectory=(cfg.steps * dense_ms) / (float(np.median(disc)) + sel_ms + L * late_ms),
         trajectory_ms_wall=wall,
+        traffic_bytes_per_launch=measured_traffic(cfg.name) if tau is None and mode == "accumulate" else None,
     )
+    if matched:
+        # The paper's matched-backend comparison: the same sparse kernel on the
+        # full causal support against the selected support (same inputs).
+        frp, fci = full_support(cfg)
+        mt = Timer()
+        for _ in range(K):
+            late_on_support(cfg, pipe, steps, out, frp, fci, mt, "full")
+        torch.cuda.synchronize()
+        full = np.array(mt.totals()["full"])
+        res["matched_full_support_ms"] = float(np.median(full))
+        res["matched_full_support_tflops"] = dflops / (full.mean() * 1e-3) / 1e12
+        res["speedup_matched_backend"] = float(np.median(full)) / late_ms
+        del frp, fci
+    res["manifest"] = manifest(cfg, steps, sched, res["tau"], mode)
     if diag:
         res.update(diagnose(cfg, pipe, steps))
-    del steps
-    torch.cuda.empty_cache()
+    if own:
+        del steps
+        torch.cuda.empty_cache()
     return res
 
 
@@ -260,6 +337,10 @@ def cpu_baseline(cfg, min_s=10.0, max_late=8):
                       f"host {os.cpu_count()} logical CPUs"}
 
 
+def rounded(r):
+    return {k: (round(v, 5) if isinstance(v, float) else v) for k, v in r.items()}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -274,6 +355,10 @@ def main():
                     help="skip the 4K, 220-head, d 96, 32-key-block workload")
     ap.add_argument("--no-diagnostics", action="store_true",
                     help="skip the retained-mass / rolling-stability diagnostics")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the 8K, 16K (threshold sweep) and 32K workloads")
+    ap.add_argument("--big-steps", type=int, default=3,
+                    help="timed trajectories of each 8K / 16K / 32K leg (one warm-up each)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this many MiB (a "
                          "known-size reference for hardware byte counters)")
@@ -310,11 +395,25 @@ def main():
     if not args.no_paper_geometry and args.config == "4k":
         for mode in ("union", "accumulate"):
             pg[mode] = measure(CONFIGS["4k-b32"], args.steps, args.warmup, mode=mode,
-                               diag=not args.no_diagnostics)
+                               diag=not args.no_diagnostics, matched=mode == "union")
             log(f"[bench] paper geometry ({mode}) {json.dumps(pg[mode])}")
         pg["grouped_query_union"] = measure(CONFIGS["4k-gqa"], args.steps, args.warmup,
                                             mode="union", diag=not args.no_diagnostics)
         log(f"[bench] grouped-query geometry (union) {json.dumps(pg['grouped_query_union'])}")
+    other = {}
+    if not args.no_other_workloads and args.config == "4k":
+        K2 = max(1, min(args.steps, args.big_steps))
+        for name in ("8k", "16k", "32k"):
+            ocfg = CONFIGS[name]
+            log(f"[bench] {name}: generating {ocfg.steps} steps of inputs")
+            steps = make_inputs(ocfg)
+            for t in sorted(ocfg.taus):
+                key = name if len(ocfg.taus) == 1 else f"{name}_tau{t}"
+                other[key] = measure(ocfg, K2, 1, tau=None if t == ocfg.tau else t, steps=steps,
+                                     diag=not args.no_diagnostics and t == ocfg.tau)
+                log(f"[bench] {key} {json.dumps(other[key])}")
+            del steps
+            torch.cuda.empty_cache()
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
@@ -351,13 +450,11 @@ def main():
                      "flops_per_launch": eff, "avg_launch_ms": round(main_res["late_ms_mean"], 5),
                      "device": device_clock()},
         "cpu_baseline": cpu,
-        "detail": {k: (round(v, 5) if isinstance(v, float) else v) for k, v in main_res.items()},
-        "paper_regime": None if pr is None else {
-            k: (round(v, 5) if isinstance(v, float) else v) for k, v in pr.items()},
-        "paper_regime_union": None if pu is None else {
-            k: (round(v, 5) if isinstance(v, float) else v) for k, v in pu.items()},
-        "paper_geometry": {m: {k: (round(v, 5) if isinstance(v, float) else v) for k, v in r.items()}
-                           for m, r in pg.items()} or None,
+        "detail": rounded(main_res),
+        "paper_regime": None if pr is None else rounded(pr),
+        "paper_regime_union": None if pu is None else rounded(pu),
+        "paper_geometry": {m: rounded(r) for m, r in pg.items()} or None,
+        "other_workloads": {m: rounded(r) for m, r in other.items()} or None,
         "context": "paper: up to 1.76x late-step speedup over FlashAttention at 4K on an RTX A6000",
     }
     print(json.dumps(line), flush=True)
