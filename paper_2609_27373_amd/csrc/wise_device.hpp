@@ -115,12 +115,20 @@ struct Sched {
 };
 
 // Host: the schedule for `heads` x `items` pieces whose heads each stream
-// kv_bytes of K/V.  Group size: every head of the XCD when 8 divides the
-// head count (measured at 4K / 32 heads / block 64: interleaving 2 heads at a
-// time keeps more K/V in L2, 112 instead of 154 MiB fetched per sparse
-// launch, but balances worse and runs 5% slower; that grid runs in about two
-// rounds of resident work-groups per XCD).  Otherwise as many heads as fit
-// about 3 MiB of the 4 MiB L2 (many heads per XCD, many rounds of work).
+// kv_bytes of K/V.  Group size:
+//  - a head of 4 MiB of K/V or more (16K and 32K tokens at d 128): as many
+//    heads as fit 16 MiB, so the rows in flight on an XCD walk the same few
+//    heads' keys in ascending order together and hit each other's tiles in
+//    L2 (measured: 32K / 32 heads, one head at a time, 8% faster sparse and
+//    4% faster dense than four interleaved heads, which fetched 16 times the
+//    algorithmic bytes; 16K, two at a time, 9% and 6%);
+//  - otherwise every head of the XCD when 8 divides the head count
+//    (measured at 4K / 32 heads / block 64: interleaving 2 heads at a time
+//    keeps more K/V in L2, 112 instead of 154 MiB fetched per sparse launch,
+//    but balances worse and runs 5% slower; that grid runs in about two
+//    rounds of resident work-groups per XCD);
+//  - otherwise as many heads as fit about 3 MiB of the 4 MiB L2 (many heads
+//    per XCD, many rounds of work).
 inline Sched make_sched(int heads, int items, size_t kv_bytes) {
   Sched s{heads, items, 1, 0};
   const int per = (heads + 7) / 8;
@@ -128,7 +136,10 @@ inline Sched make_sched(int heads, int items, size_t kv_bytes) {
   // partition only while that costs at most 10%.
   if (heads >= 8 && 80 * per <= 11 * heads) {
     s.per_xcd = per;
-    if (heads % 8 == 0) {
+    if (kv_bytes >= (size_t)(4u << 20)) {
+      const size_t fit = (size_t)(16u << 20) / kv_bytes;
+      s.group = (int)(fit > (size_t)s.per_xcd ? (size_t)s.per_xcd : fit);
+    } else if (heads % 8 == 0) {
       s.group = s.per_xcd;
     } else {
       const size_t fit = kv_bytes > 0 ? (size_t)(3u << 20) / kv_bytes : 1;
