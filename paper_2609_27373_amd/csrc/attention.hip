@@ -421,9 +421,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
         }
 #pragma unroll
         for (int u = 0; u < kMassBatch; ++u) {
-          float y = fast_exp2(x[u] - l2);
-#pragma unroll
-          for (int off = 16; off >= 1; off >>= 1) y += __shfl_xor(y, off, 64);
+          const float y = half_wave_sum(fast_exp2(x[u] - l2));
           const int e = e0 + 2 * u + hsel;
           if ((lane & 31) == 0 && e < cend) red[wave][e - c0] = y;
         }
