@@ -15,8 +15,10 @@ the same workload beside it.  Further legs, each with its own manifest
 (seed, SHA-256 of the first and last step's inputs and of the CSR): the
 paper's geometry (4K, 220 heads, d 96, 32-key blocks) under both selection
 rules, with the same sparse kernel on the full causal support beside the
-selected one (the paper's matched-backend comparison); grouped-query
-attention; and the 8K, 16K (threshold sweep) and 32K workloads.  The oracle
+selected one (the paper's matched-backend comparison); the paper's
+block-size sweep at that geometry (blocks of 16, 64 and 128 keys under the
+union rule); grouped-query attention; and the 8K, 16K (threshold sweep) and
+32K workloads.  The oracle
 (CPU, fp64) is timed on a bounded sample as a baseline only.
 
     python bench.py [--steps K] [--warmup W] [--config 4k] [--gpus 1]
@@ -369,6 +371,8 @@ def main():
     ap.add_argument("--no-paper-regime", action="store_true")
     ap.add_argument("--no-paper-geometry", action="store_true",
                     help="skip the 4K, 220-head, d 96, 32-key-block workload")
+    ap.add_argument("--no-block-sweep", action="store_true",
+                    help="skip the block-size sweep (16, 64, 128) at the paper geometry")
     ap.add_argument("--no-diagnostics", action="store_true",
                     help="skip the retained-mass / rolling-stability diagnostics")
     ap.add_argument("--no-other-workloads", action="store_true",
@@ -416,6 +420,14 @@ def main():
         pg["grouped_query_union"] = measure(CONFIGS["4k-gqa"], args.steps, args.warmup,
                                             mode="union", diag=not args.no_diagnostics)
         log(f"[bench] grouped-query geometry (union) {json.dumps(pg['grouped_query_union'])}")
+        # the paper's block-size sweep (B 16, 32, 64, 128 under the union
+        # rule, everything else fixed); B 32 is the union leg above
+        if not args.no_block_sweep:
+            for b in (16, 64, 128):
+                key = f"block{b}_union"
+                pg[key] = measure(CONFIGS[f"4k-b{b}"], args.steps, args.warmup, mode="union",
+                                  diag=not args.no_diagnostics)
+                log(f"[bench] paper geometry, block {b} (union) {json.dumps(pg[key])}")
     other = {}
     if not args.no_other_workloads and args.config == "4k":
         K2 = max(1, min(args.steps, args.big_steps))

@@ -38,9 +38,10 @@
  *  - A successful call enqueues kernels only: no allocation, memset, copy or
  *    synchronisation, so calls may be captured in a HIP graph (the graph
  *    then reads whatever the captured buffers hold at replay time).
- *  - Supported: head_dim in {64, 96, 128}; block in {32, 64, 128};
- *    seq_len % block == 0, and seq_len % 64 == 0 for block 32 (the dense
- *    kernel's key tiles); nb <= 1024 for wise_select_support,
+ *  - Supported: head_dim in {64, 96, 128}; block in {16, 32, 64, 128} (the
+ *    block sizes of the paper's block-size sweep, Appendix "Block-Size
+ *    Tradeoff"); seq_len % block == 0, and seq_len % 64 == 0 for blocks 16
+ *    and 32 (the dense kernel's key tiles); nb <= 1024 for wise_select_support,
  *    wise_select_step and wise_support_from_masks.
  *  - Support bitmasks (the union mode and the diagnostics): uint64
  *    [rows][words], words = wise_mask_words(s) = ceil(nb / 64); bit
@@ -67,7 +68,7 @@ typedef enum {
   WISE_OK = 0,
   WISE_ERR_NULL = 1,        /* a required pointer is NULL                    */
   WISE_ERR_SHAPE = 2,       /* non-positive dimension, seq_len % block != 0
-                               (% 64 for block 32), heads % kv_heads != 0,
+                               (% 64 for blocks 16, 32), heads % kv_heads != 0,
                                a size that overflows int32 indexing, or a
                                misaligned pointer                            */
   WISE_ERR_UNSUPPORTED = 3, /* head_dim or block outside the supported set   */
@@ -124,9 +125,9 @@ enum {
  *   workspace, workspace_bytes : device scratch of at least
  *             wise_mass_workspace_bytes(s) bytes, 256-byte aligned, used
  *             only when acc != NULL (then required); contents on entry are
- *             ignored.  It holds one fp32 per (query, 64-key span, or 32-key
- *             span for block 32, up to the query's tile) between the
- *             attention and its epilogue.
+ *             ignored.  It holds one fp32 per (query, 64-key span, or
+ *             block-sized span for blocks 16 and 32, up to the query's tile)
+ *             between the attention and its epilogue.
  * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with workspace NULL),
  *         WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_WORKSPACE, WISE_ERR_HIP.
  */
@@ -219,7 +220,9 @@ wise_status wise_select_support_noalloc(const wise_shape* s, const float* acc,
  *               identity.  Schedule slot s runs row row_order[s]; slots are
  *               dealt to the 8 XCDs in contiguous ranges (slot s on XCD
  *               s / (rows / 8) when rows % 8 == 0), so rows of one head placed
- *               together share an L2.
+ *               together share an L2.  Not read for block 16, where one
+ *               work-group runs the row pair (2p, 2p+1) of a head over the
+ *               union of their supports, heaviest pairs first.
  *   o         : bf16, same shape as q, written.  A row with an empty support
  *               writes zeros (and lse = -inf).
  *   lse       : fp32 [batch][heads][seq_len] or NULL.
@@ -324,7 +327,7 @@ wise_status wise_support_mass(const wise_shape* s, const float* r,
 
 /* Bytes of device workspace wise_dense_attn_accum needs when it pools block
  * masses: one fp32 per (query, E-key span up to the end of its tile of T
- * queries), E = 32 for block 32 and 64 otherwise, T = 256 for head_dim 128
+ * queries), E = block for blocks 16 and 32 and 64 otherwise, T = 256 for head_dim 128
  * when it divides seq_len, else 128 when it divides seq_len, else 64:
  * batch * heads * T * (T / E) * m (m + 1) / 2 * 4 with m = seq_len / T
  * (about half of seq_len^2 / E floats per head; 0 for an invalid shape). */

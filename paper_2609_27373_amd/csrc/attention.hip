@@ -100,7 +100,7 @@ struct WaveRows {
   f32x16_t o[G::kDTiles];    // O^T accumulator, 32 dims x 32 queries per tile
   float m;                   // running max of scale*log2(e)*s (per query)
   float l;                   // running sum over this lane's half of the keys
-  float hs[2];               // last tile's per-half sums (softmax_pv<H, true>)
+  float hs[4];               // last tile's per-part sums (softmax_pv<H, P>, P > 0)
 
   __device__ __forceinline__ void load_q(const uint16_t* qg, int q0, int lane) {
     const uint16_t* row = qg + (size_t)(q0 + (lane & 31)) * D + 8 * (lane >> 5);
@@ -141,10 +141,10 @@ struct WaveRows {
         if (key0 + score_key(t, r, h) > qi) s[t][r] = -INFINITY;
   }
 
-  // Online softmax of one tile and O^T += V^T P^T.  With kHalves the sums
-  // of this lane's probabilities over each 32-key half of the tile are kept
-  // in hs[] (the row sum then adds the halves).
-  template <int H, bool kHalves = false>
+  // Online softmax of one tile and O^T += V^T P^T.  With kParts = 2 (4) the
+  // sums of this lane's probabilities over each 32-key half (16-key quarter)
+  // of the tile are kept in hs[] (the row sum then adds the parts).
+  template <int H, int kParts = 0>
   __device__ __forceinline__ void softmax_pv(f32x16_t s[H], const uint16_t* vt, int lane, float c) {
     float mx = -INFINITY;
 #pragma unroll
@@ -174,15 +174,20 @@ struct WaveRows {
     float ts = 0.f;
 #pragma unroll
     for (int t = 0; t < H; ++t) {
-      float th = 0.f;
+      float th = 0.f, tq[2] = {0.f, 0.f};
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = fast_exp2(__builtin_fmaf(s[t][r], c, -mb));
         s[t][r] = p;
-        if constexpr (kHalves) th += p;
+        if constexpr (kParts == 4) tq[r >> 3] += p;
+        else if constexpr (kParts == 2) th += p;
         else ts += p;
       }
-      if constexpr (kHalves) {
+      if constexpr (kParts == 4) {
+        hs[2 * t] = tq[0];
+        hs[2 * t + 1] = tq[1];
+        ts += tq[0] + tq[1];
+      } else if constexpr (kParts == 2) {
         hs[t] = th;
         ts += th;
       }
@@ -210,7 +215,7 @@ struct WaveRows {
   // One tile: S^T, the causal mask when the tile reaches past this wave's
   // first query (only ever on diagonal tiles, and only instantiated for
   // them), online softmax and PV.
-  template <bool kMask, int H = 2, bool kHalves = false>
+  template <bool kMask, int H = 2, int kParts = 0>
   __device__ __forceinline__ void attend(const uint16_t* ks, const uint16_t* vt, int lane,
                                          float c, int key0, int q0) {
     f32x16_t s[H];
@@ -218,15 +223,22 @@ struct WaveRows {
     if constexpr (kMask) {
       if (key0 + 32 * H - 1 > q0) mask<H>(s, key0, q0 + (lane & 31), lane);
     }
-    softmax_pv<H, kHalves>(s, vt, lane, c);
+    softmax_pv<H, kParts>(s, vt, lane, c);
   }
 
   // log2 of the last tile's probability mass per query, unnormalised (taken
-  // against the running max m): entry 0 and 1 for the two 32-key halves
-  // (E = 32) or entry 0 for the whole tile (E = 64).  -inf for no mass.
+  // against the running max m): entries 0..3 for the four 16-key quarters
+  // (E = 16), 0 and 1 for the two 32-key halves (E = 32) or entry 0 for the
+  // whole tile (E = 64).  -inf for no mass.
   template <int E>
-  __device__ __forceinline__ void tile_log_mass(float out[2]) const {
-    if constexpr (E == 32) {
+  __device__ __forceinline__ void tile_log_mass(float out[4]) const {
+    if constexpr (E == 16) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float x = pair_sum(hs[t]);
+        out[t] = x > 0.f ? m + __builtin_log2f(x) : -INFINITY;
+      }
+    } else if constexpr (E == 32) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const float x = pair_sum(hs[t]);
@@ -299,8 +311,9 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   using G = Geo<D>;
   constexpr int kNT = NW * 64, kQT = NW * 32;
   constexpr bool kMass = BM > 0;
-  constexpr int kE = BM == 32 ? 32 : 64;            // keys per workspace entry
+  constexpr int kE = BM > 0 && BM < 64 ? BM : 64;   // keys per workspace entry
   constexpr int kEPT = kKeyTile / kE;               // entries per 64-key tile
+  constexpr int kParts = kMass ? (kE == 16 ? 4 : 2) : 0;
   // An 8-wave group fills its CU alone (two waves per SIMD), so no other
   // group runs while it waits at a barrier: it keeps two LDS tiles and stages
   // tile it+1 into the other one right after computing tile it, one barrier
@@ -330,7 +343,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   // Per-tile mass entries of this lane's query (lanes 0..31 write them).
   auto put_mass = [&](int it) {
     if constexpr (kMass) {
-      float lm[2];
+      float lm[4];
       w.template tile_log_mass<kE>(lm);
       if (lane < 32) {
 #pragma unroll
@@ -362,7 +375,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
     int it = 0;
     for (; it < nfull; ++it) {
       const int cu = it & 1;
-      w.template attend<false, 2, kMass>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
+      w.template attend<false, 2, kParts>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
                                          it * kKeyTile, q0);
       put_mass(it);
       stage_next(it);
@@ -370,7 +383,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
     for (; it < ntiles; ++it) {
       const int cu = it & 1;
       if (it * kKeyTile <= q0) {
-        w.template attend<true, 2, kMass>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
+        w.template attend<true, 2, kParts>(ks + cu * G::kKElems, vt + cu * G::kVElems, lane, c,
                                           it * kKeyTile, q0);
         put_mass(it);
       }
@@ -381,7 +394,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
       st.store(ks, vt, tid);
       __syncthreads();
       st.load(rk, rv, (it + 1) * kKeyTile, tid);
-      w.template attend<false, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+      w.template attend<false, 2, kParts>(ks, vt, lane, c, it * kKeyTile, q0);
       put_mass(it);
       __syncthreads();
     }
@@ -390,7 +403,7 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
       __syncthreads();
       if (it + 1 < ntiles) st.load(rk, rv, (it + 1) * kKeyTile, tid);
       if (it * kKeyTile <= q0) {
-        w.template attend<true, 2, kMass>(ks, vt, lane, c, it * kKeyTile, q0);
+        w.template attend<true, 2, kParts>(ks, vt, lane, c, it * kKeyTile, q0);
         put_mass(it);
       }
       __syncthreads();
@@ -399,12 +412,15 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
   w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
   if constexpr (kMass) {
     // Epilogue: entries 0 .. elast of this wave were written above (the
-    // tiles it attended); later ones hold no mass for its queries.
-    constexpr int kWPB = BM / 32;                   // waves per query block
+    // tiles it attended); later ones hold no mass for its queries.  A
+    // 16-query block is half of a wave's queries: its sums run over 16-lane
+    // rows, and each wave feeds two query blocks.
+    constexpr int kSub = BM < 32 ? 32 / BM : 1;     // query blocks per wave
+    constexpr int kWPB = BM < 32 ? 1 : BM / 32;     // waves (or wave halves) per query block
     constexpr int kQB = kQT / BM;                   // query blocks of the group
     constexpr int kBE = BM / kE;                    // entries per key block
     static_assert(kQB >= 1 && kQT % BM == 0, "mass block larger than the group");
-    __shared__ float red[NW][kMassChunk];
+    __shared__ float red[NW * kSub][kMassChunk];
     const float l2 = w.lse2();
     const int elast = (q0 + 31) / kE;
     const int nb = n / BM;
@@ -421,9 +437,14 @@ dense_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K
         }
 #pragma unroll
         for (int u = 0; u < kMassBatch; ++u) {
-          const float y = half_wave_sum(fast_exp2(x[u] - l2));
           const int e = e0 + 2 * u + hsel;
-          if ((lane & 31) == 0 && e < cend) red[wave][e - c0] = y;
+          if constexpr (kSub == 2) {
+            const float y = row16_sum(fast_exp2(x[u] - l2));
+            if ((lane & 15) == 0 && e < cend) red[2 * wave + ((lane >> 4) & 1)][e - c0] = y;
+          } else {
+            const float y = half_wave_sum(fast_exp2(x[u] - l2));
+            if ((lane & 31) == 0 && e < cend) red[wave][e - c0] = y;
+          }
         }
       }
       __syncthreads();
@@ -527,6 +548,97 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// Block-sparse attention for 16-key blocks.  A 16-query row is half a wave's
+// 32 MFMA columns, so a one-wave group owns the row pair (2p, 2p+1) of one
+// (batch, head) and walks the union of the two rows' ascending supports in
+// 32-key tiles (key blocks 2j and 2j+1 in tile j).  Each tile carries four
+// membership bits, (row 2p, block 2j), (2p, 2j+1), (2p+1, 2j), (2p+1, 2j+1):
+// a lane masks the 16-key half of the tile its row does not hold, so every
+// query attends exactly its own row's blocks.  Heavier (later) pairs of a
+// head are issued first; the row order is not used.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(sparse_waves_per_simd(D, 32))))
+sparse_pair16_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                     const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
+                     const int32_t* __restrict__ col_idx, uint16_t* __restrict__ O,
+                     float* __restrict__ lse, int n, int nb, int heads, int gq, Sched sc,
+                     float c) {
+  using G = Geo<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[32 * G::kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[32 * G::kVStride];
+  int bh, item;
+  if (!sched_slot(sc, bh, item)) return;
+  const int p = sc.items - 1 - item;          // row pair: query blocks 2p, 2p+1
+  const int qb0 = 2 * p, r0 = bh * nb + qb0;
+  const size_t hoff = (size_t)bh * n * D;
+  const int lane = threadIdx.x;
+  const int q0 = 32 * p;
+  const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
+  const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
+
+  // Cursors over the two rows; ids outside 0..qb are skipped.
+  int e0 = row_ptr[r0], end0 = row_ptr[r0 + 1];
+  int e1 = row_ptr[r0 + 1], end1 = row_ptr[r0 + 2];
+  auto peek = [&](int& e, int end, int qb) {
+    while (e < end) {
+      const int kb = col_idx[e];
+      if ((unsigned)kb <= (unsigned)qb) return kb;
+      ++e;
+    }
+    return INT32_MAX;
+  };
+  // Next tile of the union: its index and membership bits (false at the end).
+  auto next = [&](int& tile, uint32_t& bits) {
+    int a = peek(e0, end0, qb0), b = peek(e1, end1, qb0 + 1);
+    if (a == INT32_MAX && b == INT32_MAX) return false;
+    tile = min(a, b) >> 1;
+    bits = 0;
+    while (a != INT32_MAX && (a >> 1) == tile) {
+      bits |= 1u << (a & 1);
+      ++e0;
+      a = peek(e0, end0, qb0);
+    }
+    while (b != INT32_MAX && (b >> 1) == tile) {
+      bits |= 4u << (b & 1);
+      ++e1;
+      b = peek(e1, end1, qb0 + 1);
+    }
+    return true;
+  };
+
+  WaveRows<D> w;
+  w.load_q(Q + hoff, q0, lane);
+  w.reset();
+  TileStage<D, 64, true, 32> st;
+  // This lane's query is in row 2p + rs: its membership bits sit at 2 rs.
+  const int rs = (lane >> 4) & 1;
+  int tile = 0, tile_next = 0;
+  uint32_t bits = 0, bits_next = 0;
+  bool have = next(tile, bits);
+  if (have) st.load(rk, rv, 32 * tile, lane);
+  while (have) {
+    st.store(ks, vt, lane);
+    __syncthreads();
+    const bool more = next(tile_next, bits_next);
+    if (more) st.load(rk, rv, 32 * tile_next, lane);
+    f32x16_t sc[1];
+    w.template scores<1>(ks, lane, sc);
+    const uint32_t mine = bits >> (2 * rs);
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (!((mine >> (r >> 3)) & 1u)) sc[0][r] = -INFINITY;
+    if (tile == p) WaveRows<D>::template mask<1>(sc, q0, q0 + (lane & 31), lane);
+    w.template softmax_pv<1>(sc, vt, lane, c);
+    __syncthreads();
+    tile = tile_next;
+    bits = bits_next;
+    have = more;
+  }
+  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (shapes already validated by the C ABI layer).
 // ---------------------------------------------------------------------------
 template <int D, int NW, int BM>
@@ -542,6 +654,7 @@ static void launch_dense_bm(const Dims& s, const uint16_t* Q, const uint16_t* K,
                             const uint16_t* V, uint16_t* O, float* lse, float* acc, float* ws,
                             hipStream_t st) {
   if (acc == nullptr) return launch_dense_nw<D, NW, 0>(s, Q, K, V, O, lse, acc, ws, st);
+  if (s.block == 16) return launch_dense_nw<D, NW, 16>(s, Q, K, V, O, lse, acc, ws, st);
   if (s.block == 32) return launch_dense_nw<D, NW, 32>(s, Q, K, V, O, lse, acc, ws, st);
   if (s.block == 64) return launch_dense_nw<D, NW, 64>(s, Q, K, V, O, lse, acc, ws, st);
   if constexpr (NW >= 4) launch_dense_nw<D, NW, 128>(s, Q, K, V, O, lse, acc, ws, st);
@@ -585,7 +698,7 @@ int dense_query_tile(const Dims& s) {
 size_t mass_workspace_bytes(const Dims& s) {
   // Matches dense_attn_kernel: tiles of T = dense_query_tile queries,
   // entries of E keys, tile qt holding (qt+1)*T/E entries of T queries.
-  const size_t e = s.block == 32 ? 32 : 64;
+  const size_t e = s.block < 64 ? s.block : 64;
   const size_t qt = (size_t)dense_query_tile(s);
   const size_t nq = s.n / qt;
   return (size_t)s.bh * qt * (qt / e) * (nq * (nq + 1) / 2) * sizeof(float);
@@ -600,6 +713,12 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
   const int rows = s.bh * s.nb;
+  if (s.block == 16) {
+    const Sched sp = make_sched(s.bh, s.nb / 2, (size_t)s.n * D * 4 / s.gq);
+    hipLaunchKernelGGL((sparse_pair16_kernel<D>), dim3(sched_grid(sp)), dim3(64), 0, st, Q, K, V,
+                       rp, ci, (uint16_t*)o, lse, s.n, s.nb, s.heads, s.gq, sp, c);
+    return hipGetLastError();
+  }
   const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 4 / s.gq);
   const dim3 grid(sched_grid(sc));
   if (s.block == 32)

@@ -22,9 +22,10 @@ wise_status check_shape(const wise_shape* s, wise::Dims* out) {
   if (s->batch <= 0 || s->heads <= 0 || s->seq_len <= 0 || s->head_dim <= 0 || s->block <= 0)
     return WISE_ERR_SHAPE;
   if (s->head_dim != 64 && s->head_dim != 96 && s->head_dim != 128) return WISE_ERR_UNSUPPORTED;
-  if (s->block != 32 && s->block != 64 && s->block != 128) return WISE_ERR_UNSUPPORTED;
+  if (s->block != 16 && s->block != 32 && s->block != 64 && s->block != 128)
+    return WISE_ERR_UNSUPPORTED;
   if (s->seq_len % s->block != 0) return WISE_ERR_SHAPE;
-  if (s->block == 32 && s->seq_len % 64 != 0) return WISE_ERR_SHAPE;   // 64-key dense tiles
+  if (s->block < 64 && s->seq_len % 64 != 0) return WISE_ERR_SHAPE;   // 64-key dense tiles
   const int32_t kvh = s->kv_heads == 0 ? s->heads : s->kv_heads;
   if (kvh <= 0 || s->heads % kvh != 0) return WISE_ERR_SHAPE;
   if (isnan(s->scale) || isinf(s->scale)) return WISE_ERR_RANGE;
@@ -219,12 +220,12 @@ const char* wise_status_string(wise_status st) {
     case WISE_OK: return "WISE_OK: success";
     case WISE_ERR_NULL: return "WISE_ERR_NULL: a required pointer is NULL";
     case WISE_ERR_SHAPE:
-      return "WISE_ERR_SHAPE: invalid geometry, seq_len not a multiple of block (of 64 for block "
-             "32), heads not a multiple of kv_heads, size beyond int32 CSR indexing, or a "
+      return "WISE_ERR_SHAPE: invalid geometry, seq_len not a multiple of block (of 64 for blocks "
+             "16 and 32), heads not a multiple of kv_heads, size beyond int32 CSR indexing, or a "
              "misaligned pointer";
     case WISE_ERR_UNSUPPORTED:
-      return "WISE_ERR_UNSUPPORTED: head_dim must be 64/96/128, block 32/64/128, seq_len/block "
-             "<= 1024 for selection";
+      return "WISE_ERR_UNSUPPORTED: head_dim must be 64/96/128, block 16/32/64/128, "
+             "seq_len/block <= 1024 for selection";
     case WISE_ERR_RANGE: return "WISE_ERR_RANGE: tau outside (0, 1], bad scale or unknown flag bits";
     case WISE_ERR_WORKSPACE: return "WISE_ERR_WORKSPACE: workspace smaller than required";
     case WISE_ERR_HIP: return "WISE_ERR_HIP: a kernel launch failed";

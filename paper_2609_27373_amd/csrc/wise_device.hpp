@@ -72,21 +72,27 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Sum of x over the 32 lanes of this lane's half-wave, in every lane, on the
-// VALU: quad butterflies, then the half-row and row mirrors (DPP) give each
-// 16-lane row its sum, and permlane16_swap adds the two rows of the
-// half-wave.  A fixed order, so the result is bitwise reproducible.
+// Cross-lane sums on the VALU, in a fixed order (bitwise reproducible).
 template <int kCtrl>
 __device__ __forceinline__ float dpp_mov(float v) {
   return __builtin_bit_cast(float,
                             __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), kCtrl, 0xF, 0xF, true));
 }
 
-__device__ __forceinline__ float half_wave_sum(float x) {
+// Sum of x over this lane's 16-lane row, in every lane of the row: quad
+// butterflies, then the half-row and row mirrors (DPP).
+__device__ __forceinline__ float row16_sum(float x) {
   x += dpp_mov<0xB1>(x);    // quad_perm [1,0,3,2]
   x += dpp_mov<0x4E>(x);    // quad_perm [2,3,0,1]
   x += dpp_mov<0x141>(x);   // row_half_mirror
   x += dpp_mov<0x140>(x);   // row_mirror
+  return x;
+}
+
+// Sum of x over the 32 lanes of this lane's half-wave, in every lane: the
+// two 16-lane row sums added through permlane16_swap.
+__device__ __forceinline__ float half_wave_sum(float x) {
+  x = row16_sum(x);
   const uint32_t u = __builtin_bit_cast(uint32_t, x);
   auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
   return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);

@@ -114,6 +114,13 @@ CONFIGS["4k-pr"] = CONFIGS["4k"].with_(name="4k-pr", gain=4.5)
 # support density in the paper's 37-45 % band at 4K with B = 32.
 CONFIGS["4k-b32"] = WorkloadConfig("4k-b32", 1, 220, 96, 4096, 32, 12, 20, (0.95,), (6, 6),
                                    sink=True, zipf=1.2, gain=7.5, seed=5)
+# The paper's block-size sweep (Appendix C, "Block-Size Tradeoff": B in
+# {16, 32, 64, 128} with everything else fixed) at its own geometry: the
+# 4k-b32 workload with the other block sizes (same generator, seed and gain;
+# the planted blocks then span B keys each).
+for _b in (16, 64, 128):
+    CONFIGS[f"4k-b{_b}"] = CONFIGS["4k-b32"].with_(name=f"4k-b{_b}", block=_b)
+
 # Grouped-query attention with the second backbone's geometry (Appendix B:
 # 6 recurrent blocks, 32 query heads sharing 8 key-value heads; head_dim 64
 # of its Llama-3.2 base), the blocks as the batch, and the same WISE

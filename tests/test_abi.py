@@ -64,9 +64,11 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_support_capacity(S(seq_len=500)) == -1
     assert wise.wise_select_workspace_bytes(S(head_dim=80)) == 0
     assert wise.wise_support_capacity(S(block=32)) == 2 * 16 * 17 // 2
+    assert wise.wise_support_capacity(S(block=16)) == 2 * 32 * 33 // 2
     # 512 = 4 tiles of 128 queries; tile t keeps (t+1)*2 spans of 64 keys (4 of 32 keys)
     assert wise.wise_mass_workspace_bytes(S()) == 2 * 128 * 2 * (4 * 5 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(block=32)) == 2 * 128 * 4 * (4 * 5 // 2) * 4
+    assert wise.wise_mass_workspace_bytes(S(block=16)) == 2 * 128 * 8 * (4 * 5 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(seq_len=320)) == 2 * 64 * 1 * (5 * 6 // 2) * 4
     # head_dim 128: tiles of 256 queries when they divide seq_len
     assert wise.wise_mass_workspace_bytes(S(head_dim=128)) == 2 * 256 * 4 * (2 * 3 // 2) * 4
@@ -101,7 +103,8 @@ def sparse(lib, s, q=FAKE, rp=FAKE, ci=FAKE, o=FAKE):
     (dict(s=None), 1), (dict(q=None), 1), (dict(o=None), 1), (dict(acc=FAKE), 1),
     (dict(acc=FAKE, ws=FAKE, wsb=16), 5), (dict(acc=FAKE, ws=ctypes.c_void_p(4096 + 16), wsb=1 << 40), 2),
     (dict(s=S(seq_len=500)), 2), (dict(s=S(batch=0)), 2), (dict(s=S(heads=-1)), 2),
-    (dict(s=S(head_dim=80)), 3), (dict(s=S(block=16)), 3), (dict(q=MIS), 2),
+    (dict(s=S(head_dim=80)), 3), (dict(s=S(block=8)), 3), (dict(q=MIS), 2),
+    (dict(s=S(block=16, seq_len=96)), 2),
     (dict(s=S(block=32, seq_len=96)), 2), (dict(s=S(block=256)), 3),
     (dict(s=S(heads=4, kv_heads=3)), 2), (dict(s=S(kv_heads=-1)), 2), (dict(s=S(kv_heads=4)), 2),
     (dict(s=S(scale=float("inf"))), 4), (dict(s=S(scale=float("nan"))), 4),

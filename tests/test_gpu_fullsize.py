@@ -48,11 +48,12 @@ SMALL = {
 }
 
 # Flattened query heads checked whole (None: every head).  8K: XCD 0 holds
-# heads 0-5 (one fewer than the others), 54 is the last head; 4k-b32: head 26
-# closes XCD 0's short last group of one; 4k-gqa: query heads 0 and 101 read
-# key-value heads 0 and 25.
+# heads 0-5 (one fewer than the others), 54 is the last head; 4k-b32 and
+# 4k-b16: head 26 closes XCD 0's short last group of one; 4k-gqa: query heads
+# 0 and 101 read key-value heads 0 and 25.
 WHOLE = {"4k": None, "4k-pr": (3, 30), "8k": (5, 54), "16k": (0, 63), "32k": (0, 31),
-         "4k-b32": (26, 219), "4k-gqa": (0, 101), "xcd55": None, "xcd15": None}
+         "4k-b32": (26, 219), "4k-b16": (26, 219), "4k-gqa": (0, 101), "xcd55": None,
+         "xcd15": None}
 
 
 def config(name):
@@ -88,8 +89,8 @@ def selection_only(w, pipe, cfg, acc_host, tau, what):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k", "4k-b32", "4k-gqa",
-                                  "xcd55", "xcd15"])
+@pytest.mark.parametrize("name", ["4k", "4k-pr", "8k", "16k", "32k", "4k-b32", "4k-b16",
+                                  "4k-gqa", "xcd55", "xcd15"])
 def test_fullsize_trajectory(gpu_lib, name):
     w = gpu_lib
     cfg = config(name)

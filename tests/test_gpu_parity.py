@@ -58,6 +58,7 @@ SHAPES = [  # bt, h, n, d, B  (ragged: n not a multiple of 128, single block, ..
     (2, 2, 512, 128, 128), (1, 3, 384, 96, 128), (1, 1, 128, 64, 128), (1, 2, 1024, 128, 64),
     (1, 1, 64, 96, 32), (2, 2, 384, 96, 32), (1, 2, 320, 64, 32), (1, 3, 640, 128, 32),
     (1, 2, 256, 128, 64), (1, 1, 768, 128, 32),   # one and three 256-query dense tiles
+    (1, 1, 64, 96, 16), (1, 2, 256, 64, 16), (2, 1, 384, 128, 16), (1, 3, 320, 96, 16),
 ]
 
 
@@ -124,14 +125,14 @@ def test_peaky_rows(gpu_lib, d, B):
 
 
 @pytest.mark.parametrize("d,B", [(64, 64), (96, 64), (128, 64), (128, 128), (96, 128), (64, 32),
-                                 (96, 32), (128, 32)])
+                                 (96, 32), (128, 32), (64, 16), (96, 16), (128, 16)])
 def test_full_support_sparse_equals_dense(gpu_lib, d, B):
     """With every causal block in the support, R = 0 and the sparse kernel
     computes the dense result.  For blocks of 64 and 128 keys both kernels
     walk the same 64-key tiles in the same order with the same arithmetic,
-    so the outputs agree bit for bit; 32-key blocks are walked in 32-key
-    tiles (a different online-softmax grouping), so there both are held to
-    the oracle instead."""
+    so the outputs agree bit for bit; 32- and 16-key blocks are walked in
+    32-key tiles (a different online-softmax grouping), so there both are
+    held to the oracle instead."""
     w = gpu_lib
     bt, h, n = 1, 2, 768
     q, k, v = (x.cuda() for x in inputs(bt, h, n, d, seed=d + B, scale=1.5, planted=True))
@@ -182,6 +183,40 @@ def test_sparse_edge_rows(gpu_lib):
     assert_lse(lse, l_ref, "edge lse")
 
 
+def test_sparse_block16_row_pairs(gpu_lib):
+    """16-key blocks run as row pairs (2p, 2p+1) over the union of the two
+    supports: every mix of member and empty rows, blocks held by one row
+    only, both halves of a 32-key tile, and ids past a row's diagonal (block
+    2p+1 named by row 2p) must leave each row exactly its own attention."""
+    w = gpu_lib
+    bt, h, n, d, B = 1, 2, 192, 64, 16
+    q, k, v = inputs(bt, h, n, d, seed=16, scale=1.5)
+    per_head = [[], [0, 1],            # pair 0: first row empty
+                [0, 2], [],            # pair 1: second row empty
+                [], [],                # pair 2: both empty
+                [1, 3, 6, 7], [0, 5, 7],   # pair 3: row 6 names 7 (past its diagonal)
+                [8], [0, 1, 2, 3, 4, 5, 6, 7, 8, 9],
+                [10], [11]]            # pair 5: diagonal blocks only
+    rows = per_head + [[b for b in r if b % 3 != 1] for r in per_head]
+    keep = [[b for b in r if b <= i % 12] for i, r in enumerate(rows)]
+    rp = np.array([0] + list(np.cumsum([len(r) for r in rows])), np.int32)
+    ci = np.array([b for r in rows for b in r], np.int32)
+    rp_k = np.array([0] + list(np.cumsum([len(r) for r in keep])), np.int32)
+    ci_k = np.array([b for r in keep for b in r], np.int32)
+    s = w.make_shape(bt, h, n, d, B)
+    o = torch.empty_like(q, device="cuda")
+    lse = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn(s, q.cuda(), k.cuda(), v.cuda(), torch.from_numpy(rp).cuda(),
+                       torch.from_numpy(ci).cuda(), None, o, lse)
+    torch.cuda.synchronize()
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), rp_k, ci_k, B)
+    for r in (0, 3, 4, 5):             # empty rows: zeros and -inf
+        assert torch.all(o[0, 0, 16 * r:16 * r + 16] == 0)
+        assert torch.all(torch.isneginf(lse[0, 0, 16 * r:16 * r + 16]))
+    assert_attn(o, o_ref, "B16 row pairs O")
+    assert_lse(lse, l_ref, "B16 row pairs lse")
+
+
 @pytest.mark.parametrize("nb,seed", [(1, 0), (8, 1), (63, 2), (64, 3), (65, 4), (128, 5),
                                      (200, 6), (256, 7), (513, 8), (1024, 9)])
 def test_select_only_parity(gpu_lib, nb, seed):
@@ -208,11 +243,12 @@ def test_select_only_parity(gpu_lib, nb, seed):
             assert np.array_equal(sched.row_order.cpu().numpy(), O.schedule_order(rp_ref, nb))
 
 
-def test_tiny_trajectory(gpu_lib):
+@pytest.mark.parametrize("block", [64, 16])
+def test_tiny_trajectory(gpu_lib, block):
     """The whole path on the tiny workload: 4 discovery steps (all in the
     window), selection, 4 late steps; everything against the oracle."""
     from paper_2609_27373_amd.pipeline import WisePipeline
-    cfg = CONFIGS["tiny"]
+    cfg = CONFIGS["tiny"].with_(block=block)
     tr = Trajectory(cfg)
     pipe = WisePipeline.for_config(cfg)
     masses = []
@@ -279,7 +315,7 @@ def test_determinism(gpu_lib):
         assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("B", [32, 64, 128])
+@pytest.mark.parametrize("B", [16, 32, 64, 128])
 def test_sparse_ids_past_diagonal_after_the_diagonal(gpu_lib, B):
     """Ids past the diagonal that follow the diagonal block are skipped and
     the diagonal block is still attended (with its causal mask)."""

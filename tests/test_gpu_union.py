@@ -211,11 +211,12 @@ def test_retained_mass_against_probabilities(gpu_lib):
     np.testing.assert_allclose(rm[:, 1], 1.0, atol=ACC_TOL)
 
 
-def test_union_trajectory_tiny(gpu_lib):
+@pytest.mark.parametrize("block", [64, 16])
+def test_union_trajectory_tiny(gpu_lib, block):
     """Union mode end to end on the tiny workload: per-step masses on the
     GPU, union CSR bit-exact on those masses, end to end against the
     oracle's own masses (near-ties reported), and late-step attention."""
-    cfg = CONFIGS["tiny"]
+    cfg = CONFIGS["tiny"].with_(block=block)
     say(f"union trajectory {cfg.name}")
     tr = Trajectory(cfg, device="cpu")
     steps = [tr.next(torch.bfloat16) for _ in range(cfg.steps)]
@@ -278,11 +279,12 @@ def union_options(refs, qb, tau, flags):
 
 # Whole query heads checked: one in a short last XCD group at 55 and 220
 # heads (see test_gpu_fullsize), two on different key-value heads for 4k-gqa.
-UNION_WHOLE = {"4k-pr": (3, 30), "8k": (5, 54), "4k-b32": (26, 219), "4k-gqa": (0, 101)}
+UNION_WHOLE = {"4k-pr": (3, 30), "8k": (5, 54), "4k-b32": (26, 219), "4k-b16": (26, 219),
+               "4k-gqa": (0, 101)}
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("name", ["4k-pr", "8k", "4k-b32", "4k-gqa"])
+@pytest.mark.parametrize("name", ["4k-pr", "8k", "4k-b32", "4k-b16", "4k-gqa"])
 def test_union_fullsize(gpu_lib, name):
     """Full-size union mode on whole heads: every row's per-step masses
     against the oracle's, every CSR row against the oracle's union of its own

@@ -9,7 +9,7 @@ from paper_2609_27373_amd.workloads import CONFIGS, Trajectory, planted_base, re
 
 def test_configs_divide():
     for c in CONFIGS.values():
-        assert c.seq_len % c.block == 0 and c.head_dim in (64, 96, 128) and c.block in (32, 64, 128)
+        assert c.seq_len % c.block == 0 and c.head_dim in (64, 96, 128) and c.block in (16, 32, 64, 128)
         assert c.heads % c.kvh == 0
         assert 1 <= len(c.window) <= 4 and c.window[-1] == c.discovery_steps
 
