@@ -220,9 +220,7 @@ wise_status wise_select_support_noalloc(const wise_shape* s, const float* acc,
  *               identity.  Schedule slot s runs row row_order[s]; slots are
  *               dealt to the 8 XCDs in contiguous ranges (slot s on XCD
  *               s / (rows / 8) when rows % 8 == 0), so rows of one head placed
- *               together share an L2.  Not read for block 16, where one
- *               work-group runs the row pair (2p, 2p+1) of a head over the
- *               union of their supports, heaviest pairs first.
+ *               together share an L2.
  *   o         : bf16, same shape as q, written.  A row with an empty support
  *               writes zeros (and lse = -inf).
  *   lse       : fp32 [batch][heads][seq_len] or NULL.

@@ -1,11 +1,12 @@
-// attention.hip — the two attention kernels of libwise on gfx950:
+// attention.hip — the attention kernels of libwise on gfx950:
 //
 //   dense_attn_kernel   causal flash attention, O and natural-log LSE
 //                       (paper Section 3, eq. recurrent_attention), and
 //                       optionally the block-pooled attention mass
 //                       (Section 5.1, eq. block_attention_mass)
 //   sparse_attn_kernel  attention restricted to a CSR block support
-//                       (Section 5.2, eq. wise_attention)
+//   sparse_row16_kernel (Section 5.2, eq. wise_attention); the second for
+//                       16-key blocks
 //
 // Shared tile engine.  A wave owns 32 consecutive queries.  For each tile of
 // 64 keys (32 for 32-key blocks) it computes S^T = K Q^T with
@@ -253,11 +254,14 @@ struct WaveRows {
   // log2 of the row normaliser: lse / ln 2.
   __device__ __forceinline__ float lse2() const { return m + __builtin_log2f(pair_sum(l)); }
 
-  // O = O^T / l written as bf16 rows; lse in natural log.
-  __device__ __forceinline__ void finish(uint16_t* og, float* lse, int q0, int lane) const {
+  // O = O^T / l written as bf16 rows; lse in natural log.  Only the first
+  // nq of the wave's 32 query columns are written.
+  __device__ __forceinline__ void finish(uint16_t* og, float* lse, int q0, int lane,
+                                         int nq = 32) const {
     const float lt = pair_sum(l);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     const int q = q0 + (lane & 31), h = lane >> 5;
+    if ((lane & 31) >= nq) return;
     uint16_t* row = og + (size_t)q * D + 4 * h;
 #pragma unroll
     for (int t = 0; t < G::kDTiles; ++t)
@@ -548,94 +552,112 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Block-sparse attention for 16-key blocks.  A 16-query row is half a wave's
-// 32 MFMA columns, so a one-wave group owns the row pair (2p, 2p+1) of one
-// (batch, head) and walks the union of the two rows' ascending supports in
-// 32-key tiles (key blocks 2j and 2j+1 in tile j).  Each tile carries four
-// membership bits, (row 2p, block 2j), (2p, 2j+1), (2p+1, 2j), (2p+1, 2j+1):
-// a lane masks the 16-key half of the tile its row does not hold, so every
-// query attends exactly its own row's blocks.  Heavier (later) pairs of a
-// head are issued first; the row order is not used.
+// Block-sparse attention for 16-key blocks.  One one-wave work-group per
+// (batch, head, query block) row, as for 32-key blocks; the row's 16 queries
+// fill both halves of the wave's 32 MFMA columns (lanes n and n + 16 hold the
+// same query, and only the first copy is written).  A 32-key tile is any two
+// consecutive blocks of the row's support, staged as LDS rows 0-15 and
+// 16-31, so every tile key belongs to the row; a last tile with one block
+// stages it twice and masks the copy.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(sparse_waves_per_simd(D, 32))))
-sparse_pair16_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-                     const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
-                     const int32_t* __restrict__ col_idx, uint16_t* __restrict__ O,
-                     float* __restrict__ lse, int n, int nb, int heads, int gq, Sched sc,
-                     float c) {
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
+sparse_row16_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
+                    const int32_t* __restrict__ col_idx, const int32_t* __restrict__ order,
+                    uint16_t* __restrict__ O, float* __restrict__ lse, int n, int nb, int rows,
+                    int heads, int gq, Sched sc, float c) {
   using G = Geo<D>;
+  constexpr int kRowChunks = D / 8;                 // 16-byte chunks per key row
+  constexpr int kPer = 32 * kRowChunks / 64;        // chunks per lane and tensor
   __shared__ __attribute__((aligned(16))) uint16_t ks[32 * G::kKStride];
   __shared__ __attribute__((aligned(16))) uint16_t vt[32 * G::kVStride];
-  int bh, item;
-  if (!sched_slot(sc, bh, item)) return;
-  const int p = sc.items - 1 - item;          // row pair: query blocks 2p, 2p+1
-  const int qb0 = 2 * p, r0 = bh * nb + qb0;
+  int sh, sit;
+  if (!sched_slot(sc, sh, sit)) return;
+  const int row = order ? order[sh * nb + sit] : sh * nb + (nb - 1 - sit);
+  if ((unsigned)row >= (unsigned)rows) return;
+  const int bh = row / nb, qb = row % nb;
   const size_t hoff = (size_t)bh * n * D;
   const int lane = threadIdx.x;
-  const int q0 = 32 * p;
+  const int q0 = 16 * qb;
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
 
-  // Cursors over the two rows; ids outside 0..qb are skipped.
-  int e0 = row_ptr[r0], end0 = row_ptr[r0 + 1];
-  int e1 = row_ptr[r0 + 1], end1 = row_ptr[r0 + 2];
-  auto peek = [&](int& e, int end, int qb) {
+  // The row's valid ids (0..qb) in order; the last can be the diagonal.
+  int e = row_ptr[row];
+  const int end = row_ptr[row + 1];
+  auto next_id = [&]() {
     while (e < end) {
-      const int kb = col_idx[e];
+      const int kb = col_idx[e++];
       if ((unsigned)kb <= (unsigned)qb) return kb;
-      ++e;
     }
-    return INT32_MAX;
+    return -1;
   };
-  // Next tile of the union: its index and membership bits (false at the end).
-  auto next = [&](int& tile, uint32_t& bits) {
-    int a = peek(e0, end0, qb0), b = peek(e1, end1, qb0 + 1);
-    if (a == INT32_MAX && b == INT32_MAX) return false;
-    tile = min(a, b) >> 1;
-    bits = 0;
-    while (a != INT32_MAX && (a >> 1) == tile) {
-      bits |= 1u << (a & 1);
-      ++e0;
-      a = peek(e0, end0, qb0);
-    }
-    while (b != INT32_MAX && (b >> 1) == tile) {
-      bits |= 4u << (b & 1);
-      ++e1;
-      b = peek(e1, end1, qb0 + 1);
-    }
-    return true;
+  // Tile: blocks a and b (b < 0: a alone).
+  auto next_tile = [&](int& a, int& b) {
+    a = next_id();
+    b = a < 0 ? -1 : next_id();
+    return a >= 0;
   };
 
   WaveRows<D> w;
-  w.load_q(Q + hoff, q0, lane);
+  {
+    const uint16_t* qr = Q + hoff + (size_t)(q0 + (lane & 15)) * D + 8 * (lane >> 5);
+#pragma unroll
+    for (int cc = 0; cc < G::kDChunks; ++cc) w.qf[cc] = *(const u32x4_t*)(qr + 16 * cc);
+  }
   w.reset();
-  TileStage<D, 64, true, 32> st;
-  // This lane's query is in row 2p + rs: its membership bits sit at 2 rs.
-  const int rs = (lane >> 4) & 1;
-  int tile = 0, tile_next = 0;
-  uint32_t bits = 0, bits_next = 0;
-  bool have = next(tile, bits);
-  if (have) st.load(rk, rv, 32 * tile, lane);
+  // Staging: chunk i of this lane is key row r_i (0..31) of the tile, dims
+  // 8 * (ch % kRowChunks); rows 0-15 come from block a, 16-31 from block b
+  // (from a again when the tile has one block).
+  u32x4_t kr[kPer], vr[kPer];
+  auto load = [&](int a, int b) {
+    const int bb = b < 0 ? a : b;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int ch = lane + 64 * i, r = ch / kRowChunks;
+      const int key = (r < 16 ? 16 * a : 16 * bb - 16) + r;
+      const uint32_t off = (uint32_t)(key * D + (ch % kRowChunks) * 8) * 2;
+      kr[i] = buffer_load16(rk, off, 0);
+      vr[i] = buffer_load16(rv, off, 0);
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int ch = lane + 64 * i, r = ch / kRowChunks, c8 = (ch % kRowChunks) * 8;
+      *(u32x4_t*)(ks + k_lds_row(r) * G::kKStride + c8) = kr[i];
+      *(u32x4_t*)(vt + r * G::kVStride + c8) = vr[i];
+    }
+  };
+
+  int a = -1, b = -1, an = -1, bn = -1;
+  bool have = next_tile(a, b);
+  if (have) load(a, b);
+  const int qi = q0 + (lane & 15), h = lane >> 5;
   while (have) {
-    st.store(ks, vt, lane);
+    store();
     __syncthreads();
-    const bool more = next(tile_next, bits_next);
-    if (more) st.load(rk, rv, 32 * tile_next, lane);
+    const bool more = next_tile(an, bn);
+    if (more) load(an, bn);
     f32x16_t sc[1];
     w.template scores<1>(ks, lane, sc);
-    const uint32_t mine = bits >> (2 * rs);
+    if (!more) {
+      // the last tile: the diagonal block (if present) and a masked copy
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      if (!((mine >> (r >> 3)) & 1u)) sc[0][r] = -INFINITY;
-    if (tile == p) WaveRows<D>::template mask<1>(sc, q0, q0 + (lane & 31), lane);
+      for (int r = 0; r < 16; ++r) {
+        const int blk = r < 8 ? a : b;
+        const int key = 16 * blk + 8 * h + (r & 7);
+        if (blk < 0 || key > qi) sc[0][r] = -INFINITY;
+      }
+    }
     w.template softmax_pv<1>(sc, vt, lane, c);
     __syncthreads();
-    tile = tile_next;
-    bits = bits_next;
+    a = an;
+    b = bn;
     have = more;
   }
-  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane, 16);
 }
 
 // ---------------------------------------------------------------------------
@@ -713,15 +735,12 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   const auto* K = (const uint16_t*)k;
   const auto* V = (const uint16_t*)v;
   const int rows = s.bh * s.nb;
-  if (s.block == 16) {
-    const Sched sp = make_sched(s.bh, s.nb / 2, (size_t)s.n * D * 4 / s.gq);
-    hipLaunchKernelGGL((sparse_pair16_kernel<D>), dim3(sched_grid(sp)), dim3(64), 0, st, Q, K, V,
-                       rp, ci, (uint16_t*)o, lse, s.n, s.nb, s.heads, s.gq, sp, c);
-    return hipGetLastError();
-  }
   const Sched sc = make_sched(s.bh, s.nb, (size_t)s.n * D * 4 / s.gq);
   const dim3 grid(sched_grid(sc));
-  if (s.block == 32)
+  if (s.block == 16)
+    hipLaunchKernelGGL((sparse_row16_kernel<D>), grid, dim3(64), 0, st, Q, K, V, rp, ci, order,
+                       (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
+  else if (s.block == 32)
     hipLaunchKernelGGL((sparse_attn_kernel<D, 1, 32>), grid, dim3(64), 0, st, Q, K, V, rp, ci,
                        order, (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
   else if (s.block == 64)

@@ -183,20 +183,22 @@ def test_sparse_edge_rows(gpu_lib):
     assert_lse(lse, l_ref, "edge lse")
 
 
-def test_sparse_block16_row_pairs(gpu_lib):
-    """16-key blocks run as row pairs (2p, 2p+1) over the union of the two
-    supports: every mix of member and empty rows, blocks held by one row
-    only, both halves of a 32-key tile, and ids past a row's diagonal (block
-    2p+1 named by row 2p) must leave each row exactly its own attention."""
+def test_sparse_block16_rows(gpu_lib):
+    """16-key blocks run two blocks of a row per 32-key tile, the row's 16
+    queries duplicated over the wave's 32 columns: empty rows next to full
+    ones, odd block counts (a last tile with one block), consecutive and
+    distant block pairs, the diagonal in either half of the last tile, and
+    ids past a row's diagonal must leave each row exactly its own attention
+    (and the next row's outputs untouched)."""
     w = gpu_lib
     bt, h, n, d, B = 1, 2, 192, 64, 16
     q, k, v = inputs(bt, h, n, d, seed=16, scale=1.5)
-    per_head = [[], [0, 1],            # pair 0: first row empty
-                [0, 2], [],            # pair 1: second row empty
-                [], [],                # pair 2: both empty
-                [1, 3, 6, 7], [0, 5, 7],   # pair 3: row 6 names 7 (past its diagonal)
+    per_head = [[], [0, 1],            # an empty row next to a full one
+                [0, 2], [],
+                [], [],
+                [1, 3, 6, 7], [0, 5, 7],   # row 6 names 7 (past its diagonal)
                 [8], [0, 1, 2, 3, 4, 5, 6, 7, 8, 9],
-                [10], [11]]            # pair 5: diagonal blocks only
+                [10], [11]]            # diagonal blocks only
     rows = per_head + [[b for b in r if b % 3 != 1] for r in per_head]
     keep = [[b for b in r if b <= i % 12] for i, r in enumerate(rows)]
     rp = np.array([0] + list(np.cumsum([len(r) for r in rows])), np.int32)
@@ -213,8 +215,8 @@ def test_sparse_block16_row_pairs(gpu_lib):
     for r in (0, 3, 4, 5):             # empty rows: zeros and -inf
         assert torch.all(o[0, 0, 16 * r:16 * r + 16] == 0)
         assert torch.all(torch.isneginf(lse[0, 0, 16 * r:16 * r + 16]))
-    assert_attn(o, o_ref, "B16 row pairs O")
-    assert_lse(lse, l_ref, "B16 row pairs lse")
+    assert_attn(o, o_ref, "B16 rows O")
+    assert_lse(lse, l_ref, "B16 rows lse")
 
 
 @pytest.mark.parametrize("nb,seed", [(1, 0), (8, 1), (63, 2), (64, 3), (65, 4), (128, 5),
