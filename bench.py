@@ -55,15 +55,16 @@ PEAK_HBM_GBS = 8000.0
 # for one plain 256 MiB device copy (fetch x2, write x1), and the trace's
 # average kernel duration.  They hold only for the kernel sources they were
 # taken on (MEASURED_DIGEST); any other digest reports null.
-MEASURED_DIGEST = "db7950e09981bd85"
+MEASURED_DIGEST = "9c166fed022ba798"
 MEASURED = {
-    "4k": {"bytes": 202095326, "rocprof_avg_ms": 0.1705},
-    "4k-pr": {"bytes": 249549337, "rocprof_avg_ms": 0.09196},
-    "4k-b32": {"bytes": 941368031, "rocprof_avg_ms": 0.53493},
-    "4k-gqa": {"bytes": 905943036, "rocprof_avg_ms": 0.29102},
-    "8k": {"bytes": 358326555, "rocprof_avg_ms": 0.89945},
-    "16k": {"bytes": 3741344448, "rocprof_avg_ms": 4.26951},
-    "32k": {"bytes": 5134932968, "rocprof_avg_ms": 7.95472},
+    "4k": {"bytes": 202030582, "rocprof_avg_ms": 0.17574},
+    "4k-pr": {"bytes": 249471789, "rocprof_avg_ms": 0.09796},
+    "4k-b32": {"bytes": 942785061, "rocprof_avg_ms": 0.55383},
+    "4k-b16": {"bytes": 763025708, "rocprof_avg_ms": 0.87922},
+    "4k-gqa": {"bytes": 905953996, "rocprof_avg_ms": 0.30476},
+    "8k": {"bytes": 358413557, "rocprof_avg_ms": 0.93544},
+    "16k": {"bytes": 3746812397, "rocprof_avg_ms": 4.48121},
+    "32k": {"bytes": 5131935249, "rocprof_avg_ms": 8.40485},
 }
 KERNEL_SOURCES = ("attention.hip", "wise_device.hpp")
 
