@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 
 CASES = [  # bt, heads, kv_heads, n, d, B
     (2, 4, 2, 384, 64, 32), (1, 6, 3, 512, 96, 64), (1, 4, 1, 512, 128, 128),
-    (2, 8, 2, 640, 64, 64), (1, 16, 4, 256, 96, 32),
+    (2, 8, 2, 640, 64, 64), (1, 16, 4, 256, 96, 32), (2, 4, 2, 256, 96, 16),
 ]
 
 
@@ -79,18 +79,19 @@ def test_explicit_kv_heads_equal_heads_is_plain_attention(gpu_lib):
         assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("gq,d", [(2, 64), (4, 96), (8, 128), (4, 64)])
-def test_shared_kv_heads_match_repeated_kv(gpu_lib, gq, d):
-    """32-key blocks, kv_heads < heads: every query head comes out bit for bit
+@pytest.mark.parametrize("gq,d,B", [(2, 64, 32), (4, 96, 32), (8, 128, 32), (4, 64, 32),
+                                    (4, 96, 16)])
+def test_shared_kv_heads_match_repeated_kv(gpu_lib, gq, d, B):
+    """32- and 16-key blocks, kv_heads < heads: every query head comes out bit for bit
     as with its key-value head repeated explicitly (kv_heads = heads), and a
     sampled head per batch matches the oracle.  Supports: random per query
     head, with empty rows, local bands, ids past the diagonal after the
-    diagonal block, and 130 query blocks."""
+    diagonal block, and 4160 keys (130 or 260 query blocks)."""
     w = gpu_lib
-    bt, kvh, n, B = 2, 2, 32 * 130, 32
+    bt, kvh, n = 2, 2, 32 * 130
     h = gq * kvh
     nb = n // B
-    say(f"shared kv heads gq={gq} d={d} heads={h} n={n}")
+    say(f"shared kv heads gq={gq} d={d} B={B} heads={h} n={n}")
     q, k, v = (x.cuda() for x in make(bt, h, kvh, n, d, seed=7 * gq + d))
     rng = np.random.default_rng(gq * 1000 + d)
     rp, ci = [0], []
