@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define WISE_ABI_VERSION 3
+#define WISE_ABI_VERSION 4
 
 typedef enum {
   WISE_OK = 0,
@@ -122,10 +122,13 @@ enum {
  *             caller zeroes it before the first step it should sum.  Each
  *             acc row is owned by one work-group: no float atomics, bitwise
  *             deterministic.
- *   workspace, workspace_bytes : device scratch of at least
- *             wise_mass_workspace_bytes(s) bytes, 256-byte aligned, used
+ *   workspace, workspace_bytes : device scratch, 256-byte aligned, used
  *             only when acc != NULL (then required); contents on entry are
- *             ignored.  It holds one fp32 per (query, 64-key span, or
+ *             ignored.  wise_mass_workspace_bytes(s) bytes let one launch
+ *             cover every head; any smaller size down to
+ *             wise_mass_workspace_min_bytes(s) (one key-value group of
+ *             heads) runs the heads in consecutive launches of as many
+ *             whole groups as fit, with the same results bit for bit.  It holds one fp32 per (query, 64-key span, or
  *             block-sized span for blocks 16 and 32, up to the query's tile)
  *             between the attention and its epilogue.
  * Errors: WISE_ERR_NULL (q, k, v, o NULL, or acc set with workspace NULL),
@@ -330,6 +333,11 @@ wise_status wise_support_mass(const wise_shape* s, const float* r,
  * batch * heads * T * (T / E) * m (m + 1) / 2 * 4 with m = seq_len / T
  * (about half of seq_len^2 / E floats per head; 0 for an invalid shape). */
 size_t wise_mass_workspace_bytes(const wise_shape* s);
+
+/* The smallest workspace wise_dense_attn_accum accepts with acc != NULL:
+ * wise_mass_workspace_bytes(s) / (batch * heads) * (heads / kv_heads), the
+ * share of one key-value group of query heads (0 for an invalid shape). */
+size_t wise_mass_workspace_min_bytes(const wise_shape* s);
 
 /* 64-bit words per row of a support bitmask: ceil(nb / 64)
  * (-1 for an invalid shape). */

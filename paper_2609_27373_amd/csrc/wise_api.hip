@@ -68,9 +68,29 @@ wise_status wise_dense_attn_accum(const wise_shape* s, const void* q, const void
   if ((lse && !aligned(lse, 4)) || (acc && !aligned(acc, 4)) ||
       (acc && !aligned(workspace, 256)))
     return WISE_ERR_SHAPE;
-  if (acc != nullptr && workspace_bytes < wise::mass_workspace_bytes(d)) return WISE_ERR_WORKSPACE;
-  return from_hip(wise::launch_dense(d, q, k, v, o, lse, acc, acc ? workspace : nullptr,
-                                     (hipStream_t)hip_stream));
+  if (acc == nullptr)
+    return from_hip(wise::launch_dense(d, q, k, v, o, lse, nullptr, nullptr, (hipStream_t)hip_stream));
+  // The workspace is linear in the head count: when it holds fewer than all
+  // heads, the heads run in consecutive launches of as many whole key-value
+  // groups as fit (the launches share the stream, so they reuse it in
+  // turn).  Per head the work and its order are the same either way.
+  const size_t full = wise::mass_workspace_bytes(d);
+  const size_t group = full / (size_t)d.bh * (size_t)d.gq;
+  if (workspace_bytes < group) return WISE_ERR_WORKSPACE;
+  const int per = workspace_bytes >= full ? d.bh : (int)(workspace_bytes / group) * d.gq;
+  const size_t qkv_head = (size_t)d.n * d.d * 2;   // bytes of one head of q, k, v, o
+  for (int h0 = 0; h0 < d.bh; h0 += per) {
+    wise::Dims c = d;
+    c.bh = per < d.bh - h0 ? per : d.bh - h0;
+    const size_t kv0 = (size_t)(h0 / d.gq);
+    const hipError_t e = wise::launch_dense(
+        c, (const char*)q + h0 * qkv_head, (const char*)k + kv0 * qkv_head,
+        (const char*)v + kv0 * qkv_head, (char*)o + h0 * qkv_head,
+        lse ? lse + (size_t)h0 * d.n : nullptr, acc + (size_t)h0 * d.nb * d.nb, workspace,
+        (hipStream_t)hip_stream);
+    if (e != hipSuccess) return WISE_ERR_HIP;
+  }
+  return WISE_OK;
 }
 
 wise_status wise_select_support(const wise_shape* s, const float* acc, float tau, uint32_t flags,
@@ -189,6 +209,12 @@ wise_status wise_support_mass(const wise_shape* s, const float* r, const int32_t
     return WISE_ERR_SHAPE;
   return from_hip(wise::launch_support_mass(d, r, row_ptr, col_idx, row_mass, totals,
                                             (hipStream_t)hip_stream));
+}
+
+size_t wise_mass_workspace_min_bytes(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return 0;
+  return wise::mass_workspace_bytes(d) / (size_t)d.bh * (size_t)d.gq;
 }
 
 size_t wise_mass_workspace_bytes(const wise_shape* s) {

@@ -30,7 +30,8 @@ STATUS_NAMES = {0: "WISE_OK", 1: "WISE_ERR_NULL", 2: "WISE_ERR_SHAPE", 3: "WISE_
 EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_select_support_noalloc",
            "wise_sparse_attn",
            "wise_select_step", "wise_support_from_masks", "wise_mask_union", "wise_mask_overlap",
-           "wise_support_mass", "wise_mass_workspace_bytes", "wise_mask_words",
+           "wise_support_mass", "wise_mass_workspace_bytes", "wise_mass_workspace_min_bytes",
+           "wise_mask_words",
            "wise_select_workspace_bytes",
            "wise_support_capacity", "wise_status_string", "wise_abi_version")
 
@@ -96,6 +97,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wise_support_mass.restype = ctypes.c_int
     lib.wise_mass_workspace_bytes.argtypes = [S]
     lib.wise_mass_workspace_bytes.restype = ctypes.c_size_t
+    lib.wise_mass_workspace_min_bytes.argtypes = [S]
+    lib.wise_mass_workspace_min_bytes.restype = ctypes.c_size_t
     lib.wise_mask_words.argtypes = [S]
     lib.wise_mask_words.restype = ctypes.c_int32
     lib.wise_select_workspace_bytes.argtypes = [S]
@@ -151,8 +154,9 @@ def _kv_numel(s: wise_shape) -> int:
 
 def wise_dense_attn_accum(s: wise_shape, q, k, v, o, lse=None, acc=None, workspace=None,
                           stream=None) -> None:
-    """`workspace` (any dtype, at least wise_mass_workspace_bytes(s) bytes)
-    is required with `acc`; mass_workspace() allocates one."""
+    """`workspace` (any dtype) is required with `acc`: mass_workspace()
+    allocates one; wise_mass_workspace_bytes(s) bytes run one launch, any
+    size down to wise_mass_workspace_min_bytes(s) runs the heads in turn."""
     nqkv, nlse, nacc, _ = _sizes(s)
     nkv = _kv_numel(s)
     bf = torch.bfloat16
@@ -164,9 +168,13 @@ def wise_dense_attn_accum(s: wise_shape, q, k, v, o, lse=None, acc=None, workspa
         ctypes.c_size_t(ws_bytes), _stream(stream)), "wise_dense_attn_accum")
 
 
-def mass_workspace(s: wise_shape, device="cuda") -> torch.Tensor:
-    """A device buffer of wise_mass_workspace_bytes(s) bytes."""
-    return torch.empty(max(wise_mass_workspace_bytes(s), 1), dtype=torch.uint8, device=device)
+def mass_workspace(s: wise_shape, device="cuda", max_bytes=None) -> torch.Tensor:
+    """A device buffer of wise_mass_workspace_bytes(s) bytes, or of at most
+    max_bytes (not below wise_mass_workspace_min_bytes(s))."""
+    n = wise_mass_workspace_bytes(s)
+    if max_bytes is not None:
+        n = max(min(n, int(max_bytes)), wise_mass_workspace_min_bytes(s))
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
 
 
 def _capacity(s: wise_shape) -> int:
@@ -262,6 +270,10 @@ def wise_support_mass(s: wise_shape, r, row_ptr, col_idx, row_mass, totals=None,
 
 def wise_mass_workspace_bytes(s: wise_shape) -> int:
     return int(_lib().wise_mass_workspace_bytes(ctypes.byref(s)))
+
+
+def wise_mass_workspace_min_bytes(s: wise_shape) -> int:
+    return int(_lib().wise_mass_workspace_min_bytes(ctypes.byref(s)))
 
 
 def wise_mask_words(s: wise_shape) -> int:

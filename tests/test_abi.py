@@ -43,7 +43,7 @@ def test_exports(lib):
 
 
 def test_version_and_strings(lib):
-    assert wise.wise_abi_version() == 3
+    assert wise.wise_abi_version() == 4
     for st, name in wise.STATUS_NAMES.items():
         assert wise.wise_status_string(st).startswith(name)
     assert "unknown" in wise.wise_status_string(99)
@@ -74,6 +74,11 @@ def test_capacity_and_workspace(lib):
     assert wise.wise_mass_workspace_bytes(S(head_dim=128)) == 2 * 256 * 4 * (2 * 3 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(head_dim=128, seq_len=384)) == 2 * 128 * 2 * (3 * 4 // 2) * 4
     assert wise.wise_mass_workspace_bytes(S(head_dim=80)) == 0
+    # the smallest workspace: one key-value group of heads
+    assert wise.wise_mass_workspace_min_bytes(S()) == wise.wise_mass_workspace_bytes(S()) // 2
+    g = S(heads=8, kv_heads=2, batch=3)
+    assert wise.wise_mass_workspace_min_bytes(g) == wise.wise_mass_workspace_bytes(g) // 24 * 4
+    assert wise.wise_mass_workspace_min_bytes(S(head_dim=80)) == 0
     assert wise.wise_mask_words(S()) == 1
     assert wise.wise_mask_words(S(seq_len=64 * 65)) == 2
     assert wise.wise_mask_words(s4) == 4

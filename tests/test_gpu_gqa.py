@@ -140,3 +140,36 @@ def test_shared_kv_heads_match_repeated_kv(gpu_lib, gq, d, B):
         o_ref, l_ref = O.sparse_attention(qh, kh, vh, rpv, valid, B)
         assert_attn(o_g[b, hh], o_ref[0, 0], f"head {bh} O")
         assert_lse(l_g[b, hh], l_ref[0, 0], f"head {bh} lse")
+
+
+@pytest.mark.parametrize("B", [32, 16])
+def test_mass_workspace_smaller_than_all_heads(gpu_lib, B):
+    """A mass workspace smaller than wise_mass_workspace_bytes runs the heads
+    in consecutive launches of whole key-value groups; O, LSE and the
+    accumulator come out bit for bit as with one launch, chunks crossing
+    batch boundaries included, and the accumulator matches the oracle."""
+    w = gpu_lib
+    bt, h, kvh, n, d = 3, 8, 2, 384, 96
+    nb = n // B
+    q, k, v = (x.cuda() for x in make(bt, h, kvh, n, d, seed=77 + B))
+    s = w.make_shape(bt, h, n, d, B, kv_heads=kvh)
+    full, least = w.wise_mass_workspace_bytes(s), w.wise_mass_workspace_min_bytes(s)
+    say(f"workspace full {full} B, one group {least} B")
+    outs = []
+    for size in (full, least, 2 * least + least // 2):      # 1, 6 and 3 launches
+        o = torch.empty_like(q)
+        lse = torch.empty((bt, h, n), device="cuda")
+        acc = torch.zeros((bt, h, nb, nb), device="cuda")
+        ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+        w.wise_dense_attn_accum(s, q, k, v, o, lse, acc, ws)
+        torch.cuda.synchronize()
+        outs.append((o, lse, acc))
+    for o, lse, acc in outs[1:]:
+        assert torch.equal(o, outs[0][0]) and torch.equal(lse, outs[0][1])
+        assert torch.equal(acc, outs[0][2])
+    ref = O.block_mass(f64(q), O.expand_kv(f64(k), h), B)
+    assert np.abs(f64(outs[1][2]) - ref).max() <= ACC_TOL
+    with pytest.raises(w.WiseError):
+        w.wise_dense_attn_accum(s, q, k, v, torch.empty_like(q), None,
+                                torch.zeros((bt, h, nb, nb), device="cuda"),
+                                torch.empty(least - 256, dtype=torch.uint8, device="cuda"))
