@@ -273,6 +273,8 @@ def measure(cfg, K, W, tau=None, mode="accumulate", diag=False, steps=None, matc
     late_ms, dense_ms, sel_ms = float(np.median(late)), float(np.median(dense)), float(np.median(sel))
     res = dict(
         workload=cfg.name, mode=mode, tau=float(tau if tau is not None else cfg.tau),
+        late_kernel=("sparse_group_kernel" if pipe.grouped else
+                     "sparse_row16_kernel" if cfg.block == 16 else "sparse_attn_kernel"),
         shape=f"batch {cfg.batch}, {cfg.heads} heads" + (f" over {cfg.kvh} kv heads" if cfg.grouped else "")
               + f", d {cfg.head_dim}, seq {cfg.seq_len}, block {cfg.block}, {cfg.discovery_steps} discovery "
               f"+ {cfg.late_steps} late steps",
@@ -475,7 +477,7 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "traffic": measured_traffic(cfg.name) if args.tau is None else None,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
-                     "kernel": "sparse_attn_kernel",
+                     "kernel": main_res["late_kernel"],
                      "flops_per_launch": eff, "avg_launch_ms": round(main_res["late_ms_mean"], 5),
                      "avg_launch_ms_rocprof": measured(cfg.name, "rocprof_avg_ms") if args.tau is None else None,
                      "device": device_clock()},

@@ -552,6 +552,132 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// Block-sparse attention for 64-key blocks over groups of consecutive rows:
+// the dense kernel's work-group (NW waves, 32 NW queries: 4 rows at head_dim
+// 128, 2 otherwise) walks the ascending union of its rows' supports in
+// 64-key tiles, staging each tile once for all its waves, and each wave
+// attends only the tiles its own row holds (its diagonal block masked), so
+// every row gets exactly its own attention.  Where consecutive rows' supports
+// nearly coincide (dense supports) the union adds few tiles and every staged
+// tile feeds 2-4 times the queries of the one-row group; where they differ,
+// the union walk costs more than it saves.  The membership of each row and
+// the union are built in LDS as bitmasks (up to 1024 key blocks).
+// ---------------------------------------------------------------------------
+constexpr int kGroupMaskWords = 16;
+
+template <int D, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                    const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
+                    const int32_t* __restrict__ col_idx, uint16_t* __restrict__ O,
+                    float* __restrict__ lse, int n, int nb, int heads, int gq, Sched sc,
+                    float c) {
+  using G = Geo<D>;
+  constexpr int kNT = NW * 64, kQT = NW * 32, kR = kQT / kKeyTile;   // rows per group
+  constexpr int kW = kGroupMaskWords;
+  constexpr int kBufs = NW == 8 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) uint16_t ks[kBufs * G::kKElems];
+  __shared__ __attribute__((aligned(16))) uint16_t vt[kBufs * G::kVElems];
+  __shared__ unsigned long long rmask[kR][kW];   // membership per row of the group
+  __shared__ unsigned long long umask[kW];       // their union
+  int bh, item;
+  if (!sched_slot(sc, bh, item)) return;
+  const int qt = sc.items - 1 - item;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qbase = qt * kQT, q0 = qbase + 32 * wave;
+  const int qb0 = qt * kR, mine = wave >> 1;      // the group's first row; this wave's row
+  const size_t hoff = (size_t)bh * n * D;
+  const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
+  const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
+  const int words = (nb + 63) >> 6;
+
+  WaveRows<D> w;
+  w.load_q(Q + hoff, q0, lane);
+  w.reset();
+  for (int i = tid; i < (kR + 1) * kW; i += kNT) {
+    if (i < kR * kW) rmask[i / kW][i % kW] = 0ull;
+    else umask[i - kR * kW] = 0ull;
+  }
+  __syncthreads();
+  // Valid ids (0..qb) of every row of the group into the bitmasks.
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int row = bh * nb + qb0 + r, qb = qb0 + r;
+    const int beg = row_ptr[row], end = row_ptr[row + 1];
+    for (int e = beg + tid; e < end; e += kNT) {
+      const int kb = col_idx[e];
+      if ((unsigned)kb <= (unsigned)qb) {
+        const unsigned long long bit = 1ull << (kb & 63);
+        atomicOr(&rmask[r][kb >> 6], bit);
+        atomicOr(&umask[kb >> 6], bit);
+      }
+    }
+  }
+  __syncthreads();
+  // Ascending set bits of the union (the same sequence in every wave).
+  int wi = 0;
+  unsigned long long cur = words > 0 ? umask[0] : 0ull;
+  auto next = [&](int& kb) {
+    while (cur == 0ull) {
+      if (++wi >= words) return false;
+      cur = umask[wi];
+    }
+    kb = (wi << 6) + __builtin_ctzll(cur);
+    cur &= cur - 1ull;
+    return true;
+  };
+  auto member = [&](int kb) { return (rmask[mine][kb >> 6] >> (kb & 63)) & 1ull; };
+  auto attend = [&](const uint16_t* kt, const uint16_t* vv, int kb) {
+    if (!member(kb)) return;
+    if (kb * kKeyTile + kKeyTile - 1 > q0) w.template attend<true>(kt, vv, lane, c, kb * kKeyTile, q0);
+    else w.template attend<false>(kt, vv, lane, c, kb * kKeyTile, q0);
+  };
+
+  TileStage<D, kNT, true> st;
+  int kb = 0, kb1 = 0, kb2 = 0;
+  bool have = next(kb);
+  if (have) st.load(rk, rv, kb * kKeyTile, tid);
+  if constexpr (kBufs == 2) {
+    // Double-buffered as the dense 8-wave group: tile i+1 is stored into the
+    // idle buffer right after tile i is computed, one barrier per tile.
+    if (have) {
+      st.store(ks, vt, tid);
+      bool h1 = next(kb1);
+      if (h1) st.load(rk, rv, kb1 * kKeyTile, tid);
+      __syncthreads();
+      for (int it = 0;; ++it) {
+        const int cu = it & 1;
+        attend(ks + cu * G::kKElems, vt + cu * G::kVElems, kb);
+        bool h2 = false;
+        if (h1) {
+          const int nx = (it + 1) & 1;
+          st.store(ks + nx * G::kKElems, vt + nx * G::kVElems, tid);
+          h2 = next(kb2);
+          if (h2) st.load(rk, rv, kb2 * kKeyTile, tid);
+        }
+        __syncthreads();
+        if (!h1) break;
+        kb = kb1;
+        kb1 = kb2;
+        h1 = h2;
+      }
+    }
+  } else {
+    while (have) {
+      st.store(ks, vt, tid);
+      __syncthreads();
+      const bool more = next(kb1);
+      if (more) st.load(rk, rv, kb1 * kKeyTile, tid);
+      attend(ks, vt, kb);
+      __syncthreads();
+      kb = kb1;
+      have = more;
+    }
+  }
+  w.finish(O + hoff, lse ? lse + (size_t)bh * n : nullptr, q0, lane);
+}
+
+// ---------------------------------------------------------------------------
 // Block-sparse attention for 16-key blocks.  One one-wave work-group per
 // (batch, head, query block) row, as for 32-key blocks; the row's 16 queries
 // fill both halves of the wave's 32 MFMA columns (lanes n and n + 16 hold the
@@ -749,6 +875,34 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   else
     hipLaunchKernelGGL((sparse_attn_kernel<D, 4, 64>), grid, dim3(256), 0, st, Q, K, V, rp, ci,
                        order, (uint16_t*)o, lse, s.n, s.nb, rows, s.heads, s.gq, sc, c);
+  return hipGetLastError();
+}
+
+template <int D, int NW>
+static void launch_group_nw(const Dims& s, const void* q, const void* k, const void* v,
+                            const int32_t* rp, const int32_t* ci, void* o, float* lse,
+                            hipStream_t st) {
+  const Sched sc = make_sched(s.bh, s.n / (NW * 32), (size_t)s.n * D * 4 / s.gq);
+  hipLaunchKernelGGL((sparse_group_kernel<D, NW>), dim3(sched_grid(sc)), dim3(NW * 64), 0, st,
+                     (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, rp, ci,
+                     (uint16_t*)o, lse, s.n, s.nb, s.heads, s.gq, sc, s.scale * kLog2e);
+}
+
+int sparse_group_rows(const Dims& s) {
+  if (s.block != 64 || s.nb > 64 * kGroupMaskWords) return 0;
+  const int qt = dense_query_tile(s);
+  return qt >= 128 ? qt / 64 : 0;
+}
+
+hipError_t launch_sparse_grouped(const Dims& s, const void* q, const void* k, const void* v,
+                                 const int32_t* rp, const int32_t* ci, void* o, float* lse,
+                                 hipStream_t st) {
+  const int rows = sparse_group_rows(s);
+  if (rows == 4 && s.d == 128) launch_group_nw<128, 8>(s, q, k, v, rp, ci, o, lse, st);
+  else if (rows == 2 && s.d == 128) launch_group_nw<128, 4>(s, q, k, v, rp, ci, o, lse, st);
+  else if (rows == 2 && s.d == 96) launch_group_nw<96, 4>(s, q, k, v, rp, ci, o, lse, st);
+  else if (rows == 2 && s.d == 64) launch_group_nw<64, 4>(s, q, k, v, rp, ci, o, lse, st);
+  else return launch_sparse(s, q, k, v, rp, ci, nullptr, o, lse, st);
   return hipGetLastError();
 }
 

@@ -144,6 +144,27 @@ wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k, 
                                       (hipStream_t)hip_stream));
 }
 
+wise_status wise_sparse_attn_grouped(const wise_shape* s, const void* q, const void* k,
+                                     const void* v, const int32_t* row_ptr,
+                                     const int32_t* col_idx, void* o, float* lse,
+                                     void* hip_stream) {
+  wise::Dims d;
+  wise_status st = check_shape(s, &d);
+  if (st != WISE_OK) return st;
+  if ((st = check_qkvo(q, k, v, o)) != WISE_OK) return st;
+  if (!row_ptr || !col_idx) return WISE_ERR_NULL;
+  if (!aligned(row_ptr, 4) || !aligned(col_idx, 4) || (lse && !aligned(lse, 4)))
+    return WISE_ERR_SHAPE;
+  return from_hip(wise::launch_sparse_grouped(d, q, k, v, row_ptr, col_idx, o, lse,
+                                              (hipStream_t)hip_stream));
+}
+
+int32_t wise_sparse_group_rows(const wise_shape* s) {
+  wise::Dims d;
+  if (check_shape(s, &d) != WISE_OK) return -1;
+  return wise::sparse_group_rows(d);
+}
+
 wise_status wise_select_step(const wise_shape* s, const float* r, float tau, uint64_t* mask,
                              void* hip_stream) {
   wise::Dims d;

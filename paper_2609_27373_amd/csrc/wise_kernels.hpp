@@ -24,6 +24,13 @@ int dense_query_tile(const Dims& s);   // queries per dense work-group: 64, 128 
 hipError_t launch_sparse(const Dims& s, const void* q, const void* k, const void* v,
                          const int32_t* row_ptr, const int32_t* col_idx, const int32_t* order,
                          void* o, float* lse, hipStream_t st);
+// Block 64: work-groups of 2 or 4 consecutive rows over the union of their
+// supports (sparse_group_rows(s) rows per group; 0: not available, and
+// launch_sparse_grouped runs launch_sparse instead).
+int sparse_group_rows(const Dims& s);
+hipError_t launch_sparse_grouped(const Dims& s, const void* q, const void* k, const void* v,
+                                 const int32_t* row_ptr, const int32_t* col_idx, void* o,
+                                 float* lse, hipStream_t st);
 hipError_t launch_select(const Dims& s, const float* acc, float tau, uint32_t flags,
                          int32_t* row_ptr, int32_t* col_idx, int32_t* row_order, void* ws,
                          hipStream_t st);

@@ -28,7 +28,7 @@ STATUS_NAMES = {0: "WISE_OK", 1: "WISE_ERR_NULL", 2: "WISE_ERR_SHAPE", 3: "WISE_
 
 # Every symbol include/wise.h declares.
 EXPORTS = ("wise_dense_attn_accum", "wise_select_support", "wise_select_support_noalloc",
-           "wise_sparse_attn",
+           "wise_sparse_attn", "wise_sparse_attn_grouped", "wise_sparse_group_rows",
            "wise_select_step", "wise_support_from_masks", "wise_mask_union", "wise_mask_overlap",
            "wise_support_mass", "wise_mass_workspace_bytes", "wise_mass_workspace_min_bytes",
            "wise_mask_words",
@@ -84,6 +84,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.wise_select_support_noalloc.restype = ctypes.c_int
     lib.wise_sparse_attn.argtypes = [S, P, P, P, P, P, P, P, P, P]
     lib.wise_sparse_attn.restype = ctypes.c_int
+    lib.wise_sparse_attn_grouped.argtypes = [S, P, P, P, P, P, P, P, P]
+    lib.wise_sparse_attn_grouped.restype = ctypes.c_int
+    lib.wise_sparse_group_rows.argtypes = [S]
+    lib.wise_sparse_group_rows.restype = ctypes.c_int32
     lib.wise_select_step.argtypes = [S, P, ctypes.c_float, P, P]
     lib.wise_select_step.restype = ctypes.c_int
     lib.wise_support_from_masks.argtypes = [S, P, ctypes.c_int32, ctypes.c_uint32, P, P, P, P,
@@ -218,6 +222,22 @@ def wise_sparse_attn(s: wise_shape, q, k, v, row_ptr, col_idx, row_order, o, lse
         _ptr(row_ptr, i32, "row_ptr", rows + 1), _ptr(col_idx, i32, "col_idx"),
         _ptr(row_order, i32, "row_order", rows), _ptr(o, bf, "o", nqkv),
         _ptr(lse, torch.float32, "lse", nlse), _stream(stream)), "wise_sparse_attn")
+
+
+def wise_sparse_attn_grouped(s: wise_shape, q, k, v, row_ptr, col_idx, o, lse=None,
+                             stream=None) -> None:
+    nqkv, nlse, _, rows = _sizes(s)
+    nkv = _kv_numel(s)
+    bf, i32 = torch.bfloat16, torch.int32
+    _check(_lib().wise_sparse_attn_grouped(
+        ctypes.byref(s), _ptr(q, bf, "q", nqkv), _ptr(k, bf, "k", nkv), _ptr(v, bf, "v", nkv),
+        _ptr(row_ptr, i32, "row_ptr", rows + 1), _ptr(col_idx, i32, "col_idx"),
+        _ptr(o, bf, "o", nqkv), _ptr(lse, torch.float32, "lse", nlse), _stream(stream)),
+        "wise_sparse_attn_grouped")
+
+
+def wise_sparse_group_rows(s: wise_shape) -> int:
+    return int(_lib().wise_sparse_group_rows(ctypes.byref(s)))
 
 
 def _mask_elems(s: wise_shape, n: int = 1) -> int:

@@ -43,7 +43,7 @@ def test_exports(lib):
 
 
 def test_version_and_strings(lib):
-    assert wise.wise_abi_version() == 4
+    assert wise.wise_abi_version() == 5
     for st, name in wise.STATUS_NAMES.items():
         assert wise.wise_status_string(st).startswith(name)
     assert "unknown" in wise.wise_status_string(99)
@@ -138,7 +138,21 @@ def test_select_validation(lib, case, status):
 ])
 def test_sparse_validation(lib, case, status):
     s = case.pop("s", S())
-    assert sparse(lib, s, **case) == status
+    assert sparse(lib, s, **dict(case)) == status
+    g = dict(case)
+    assert lib.wise_sparse_attn_grouped(sh(s), g.get("q", FAKE), FAKE, FAKE, g.get("rp", FAKE),
+                                        g.get("ci", FAKE), g.get("o", FAKE), None, None) == status
+
+
+def test_sparse_group_rows(lib):
+    assert wise.wise_sparse_group_rows(S(head_dim=128, seq_len=1024)) == 4   # 256-query groups
+    assert wise.wise_sparse_group_rows(S(head_dim=128, seq_len=640)) == 2    # 128 divides, 256 not
+    assert wise.wise_sparse_group_rows(S(head_dim=96)) == 2
+    assert wise.wise_sparse_group_rows(S(head_dim=64, seq_len=320)) == 0     # 64-query tiles
+    assert wise.wise_sparse_group_rows(S(block=32)) == 0
+    assert wise.wise_sparse_group_rows(S(block=128)) == 0
+    assert wise.wise_sparse_group_rows(S(seq_len=64 * 2048)) == 0            # > 1024 key blocks
+    assert wise.wise_sparse_group_rows(S(seq_len=500)) == -1
 
 
 MIS8 = ctypes.c_void_p(4096 + 4)    # 4-byte but not 8-byte aligned

@@ -159,6 +159,62 @@ def test_full_support_sparse_equals_dense(gpu_lib, d, B):
         assert_lse(ls, l_ref, "full-support sparse lse")
 
 
+@pytest.mark.parametrize("bt,h,kvh,n,d,B", [
+    (1, 2, 2, 1024, 128, 64), (2, 3, 3, 640, 128, 64), (1, 4, 2, 512, 96, 64), (2, 2, 1, 384, 64, 64),
+    (1, 2, 2, 512, 96, 32), (1, 2, 2, 512, 128, 128), (1, 2, 2, 320, 64, 64),
+])
+def test_grouped_equals_rows(gpu_lib, bt, h, kvh, n, d, B):
+    """wise_sparse_attn_grouped (block 64: 4 or 2 consecutive rows per group
+    over the union of their supports) gives wise_sparse_attn's outputs bit
+    for bit, and both match the oracle: random rows, empty rows, local bands,
+    full rows, rows without their diagonal block and ids past the diagonal.
+    Other blocks, and 64-query tiles (n = 320), run the one-row kernel."""
+    w = gpu_lib
+    nb = n // B
+    s = w.make_shape(bt, h, n, d, B, kv_heads=kvh)
+    say(f"grouped vs rows bt={bt} h={h} kvh={kvh} n={n} d={d} B={B}: "
+        f"{w.wise_sparse_group_rows(s)} rows per group")
+    g = torch.Generator().manual_seed(n + d + B)
+    q = (torch.randn((bt, h, n, d), generator=g) * 1.5).to(torch.bfloat16)
+    k = torch.randn((bt, kvh, n, d), generator=g).to(torch.bfloat16)
+    v = torch.randn((bt, kvh, n, d), generator=g).to(torch.bfloat16)
+    rng = np.random.default_rng(n * d + B)
+    rp, ci, keep = [0], [], []
+    for _ in range(bt * h):
+        for qb in range(nb):
+            u = rng.random()
+            if u < 0.1:
+                ids = []
+            elif u < 0.25:
+                ids = list(range(max(0, qb - 3), qb + 1))
+            elif u < 0.45:
+                ids = list(range(qb + 1))
+            elif u < 0.55:
+                ids = sorted(set(np.nonzero(rng.random(qb + 1) < 0.5)[0].tolist()) - {qb})
+            else:
+                ids = sorted(set(np.nonzero(rng.random(qb + 1) < 0.6)[0].tolist()) | {qb})
+            keep.append(list(ids))
+            if u > 0.9:
+                ids = ids + [qb + 1 + int(rng.integers(3))]     # past the diagonal
+            ci.extend(ids)
+            rp.append(len(ci))
+    rp_t = torch.tensor(rp, dtype=torch.int32, device="cuda")
+    ci_t = torch.tensor(ci, dtype=torch.int32, device="cuda")
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    o_r, o_g = torch.empty_like(qd), torch.empty_like(qd)
+    l_r, l_g = (torch.empty((bt, h, n), device="cuda") for _ in range(2))
+    w.wise_sparse_attn(s, qd, kd, vd, rp_t, ci_t, None, o_r, l_r)
+    w.wise_sparse_attn_grouped(s, qd, kd, vd, rp_t, ci_t, o_g, l_g)
+    torch.cuda.synchronize()
+    assert torch.equal(o_r, o_g) and torch.equal(l_r, l_g)
+    rp_k = np.array([0] + list(np.cumsum([len(r) for r in keep])), np.int32)
+    ci_k = np.array([b for r in keep for b in r], np.int32)
+    o_ref, l_ref = O.sparse_attention(f64(q), O.expand_kv(f64(k), h), O.expand_kv(f64(v), h),
+                                      rp_k, ci_k, B)
+    assert_attn(o_g, o_ref, "grouped O")
+    assert_lse(l_g, l_ref, "grouped lse")
+
+
 def test_sparse_edge_rows(gpu_lib):
     """Empty rows give O = 0 and lse = -inf; ids past the diagonal are skipped."""
     w = gpu_lib
