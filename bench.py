@@ -55,16 +55,16 @@ PEAK_HBM_GBS = 8000.0
 # for one plain 256 MiB device copy (fetch x2, write x1), and the trace's
 # average kernel duration.  They hold only for the kernel sources they were
 # taken on (MEASURED_DIGEST); any other digest reports null.
-MEASURED_DIGEST = "9c166fed022ba798"
+MEASURED_DIGEST = "7b5ff3d443b6ba80"
 MEASURED = {
-    "4k": {"bytes": 202030582, "rocprof_avg_ms": 0.17574},
-    "4k-pr": {"bytes": 249471789, "rocprof_avg_ms": 0.09796},
-    "4k-b32": {"bytes": 942785061, "rocprof_avg_ms": 0.55383},
-    "4k-b16": {"bytes": 763025708, "rocprof_avg_ms": 0.87922},
-    "4k-gqa": {"bytes": 905953996, "rocprof_avg_ms": 0.30476},
-    "8k": {"bytes": 358413557, "rocprof_avg_ms": 0.93544},
-    "16k": {"bytes": 3746812397, "rocprof_avg_ms": 4.48121},
-    "32k": {"bytes": 5131935249, "rocprof_avg_ms": 8.40485},
+    "4k": {"bytes": 193906886, "rocprof_avg_ms": 0.15474},
+    "4k-pr": {"bytes": 249071847, "rocprof_avg_ms": 0.09529},
+    "4k-b32": {"bytes": 941281634, "rocprof_avg_ms": 0.53538},
+    "4k-b16": {"bytes": 763097722, "rocprof_avg_ms": 0.87781},
+    "4k-gqa": {"bytes": 905818382, "rocprof_avg_ms": 0.29075},
+    "8k": {"bytes": 363896338, "rocprof_avg_ms": 0.86717},
+    "16k": {"bytes": 3733876052, "rocprof_avg_ms": 4.32854},
+    "32k": {"bytes": 5186282415, "rocprof_avg_ms": 8.13629},
 }
 KERNEL_SOURCES = ("attention.hip", "wise_device.hpp")
 
