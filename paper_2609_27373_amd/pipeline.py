@@ -20,13 +20,18 @@ Two late-step kernels compute the same outputs (late_kernel):
              the union of their supports (faster where supports are dense)
   "auto"     grouped where the library offers it and the selected support's
              density (nnz over the causal block pairs) is at least
-             group_density, rows otherwise; select() then reads nnz back
-             (one synchronisation per selection; a select() under graph
-             capture keeps the previous choice)
+             group_density, rows otherwise.  The first select() reads nnz
+             back (one synchronisation); later ones copy it to pinned host
+             memory asynchronously, and the choice follows when the copy
+             has landed (checked without waiting at each select() and late
+             step), so the host never waits on the device again.  Both
+             kernels give the same outputs, so when the switch happens does
+             not change any result.  A select() under graph capture keeps
+             the current choice.
 
 Buffers are allocated once per trajectory (torch device memory); every call
-enqueues on the current stream and returns (select() in "auto" mode waits
-for the selection to read its size).
+enqueues on the current stream and returns (except the first select() in
+"auto" mode, which waits for the selection to read its size).
 """
 
 from __future__ import annotations
@@ -72,6 +77,10 @@ class WisePipeline:
         self.late_kernel = late_kernel
         self.group_density = float(group_density)
         self.grouped = late_kernel == "grouped"
+        self._auto = (late_kernel == "auto" and wise.wise_sparse_group_rows(self.shape) > 0)
+        self._decided = False
+        self._nnz_host = torch.empty(1, dtype=torch.int32, pin_memory=True) if self._auto else None
+        self._nnz_event = None
 
     @classmethod
     def for_config(cls, cfg, tau=None, **kw):
@@ -108,17 +117,30 @@ class WisePipeline:
             self.schedule.from_masks(self.masks, self.filled, self.flags)
         else:
             self.schedule.select(self.acc, self.tau, self.flags)
-        # Under graph capture the size cannot be read back: the choice of the
-        # last eager selection stands (both kernels give the same outputs).
-        if self.late_kernel == "auto" and not torch.cuda.is_current_stream_capturing():
-            self.grouped = False
-            if wise.wise_sparse_group_rows(self.shape) > 0:
-                density = self.schedule.nnz() / wise.wise_support_capacity(self.shape)
-                self.grouped = density >= self.group_density
+        if self._auto and not torch.cuda.is_current_stream_capturing():
+            if not self._decided:
+                self._decide(self.schedule.nnz())
+                self._decided = True
+            else:
+                self._poll()
+                self._nnz_host.copy_(self.schedule.row_ptr[-1:], non_blocking=True)
+                self._nnz_event = torch.cuda.Event()
+                self._nnz_event.record()
         return self.schedule
+
+    def _decide(self, nnz: int):
+        self.grouped = nnz / wise.wise_support_capacity(self.shape) >= self.group_density
+
+    def _poll(self):
+        """Take up the last asynchronously copied support size if it has landed."""
+        if self._nnz_event is not None and self._nnz_event.query():
+            self._decide(int(self._nnz_host[0]))
+            self._nnz_event = None
 
     def late_step(self, q, k, v, out, lse=None, ordered=True):
         s = self.schedule
+        if self._nnz_event is not None and not torch.cuda.is_current_stream_capturing():
+            self._poll()
         if self.grouped:
             wise.wise_sparse_attn_grouped(self.shape, q, k, v, s.row_ptr, s.col_idx, out, lse)
         else:
