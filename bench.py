@@ -271,6 +271,11 @@ def measure(cfg, K, W, tau=None, mode="accumulate", diag=False, steps=None, matc
     sel = np.array(tt["select"])
     L = cfg.late_steps
     late_ms, dense_ms, sel_ms = float(np.median(late)), float(np.median(dense)), float(np.median(sel))
+    # Average launch durations: an event pair spans the device waiting on the
+    # host when the host stalls between recording the first event and the
+    # launch (tens of ms, rare), so pairs above 1.5x the median are left out
+    # of the averages (and counted).
+    late_kept, dense_kept = late[late <= 1.5 * late_ms], dense[dense <= 1.5 * dense_ms]
     res = dict(
         workload=cfg.name, mode=mode, tau=float(tau if tau is not None else cfg.tau),
         late_kernel=("sparse_group_kernel" if pipe.grouped else
@@ -280,12 +285,14 @@ def measure(cfg, K, W, tau=None, mode="accumulate", diag=False, steps=None, matc
               f"+ {cfg.late_steps} late steps",
         timed_trajectories=K, warmup_trajectories=W,
         density=metrics.density(rp, cfg.nb, bh), nnz=int(rp[-1]),
-        late_ms=late_ms, late_ms_mean=float(late.mean()),
+        late_ms=late_ms, late_ms_mean=float(late_kept.mean()),
         late_ms_iqr=[float(np.percentile(late, 25)), float(np.percentile(late, 75))],
-        late_tflops=eff / (late.mean() * 1e-3) / 1e12,
-        pct_bf16_peak=100 * eff / (late.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        late_stalled_pairs=int(late.size - late_kept.size),
+        late_tflops=eff / (late_kept.mean() * 1e-3) / 1e12,
+        pct_bf16_peak=100 * eff / (late_kept.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         eff_flops_per_late_step=eff,
-        dense_ms=dense_ms, dense_tflops=dflops / (dense.mean() * 1e-3) / 1e12,
+        dense_ms=dense_ms, dense_tflops=dflops / (dense_kept.mean() * 1e-3) / 1e12,
+        dense_stalled_pairs=int(dense.size - dense_kept.size),
         select_ms=sel_ms, discovery_ms=float(np.median(disc)),
         speedup_prepared=dense_ms / late_ms,
         speedup_setup_inclusive=(L * dense_ms) / (sel_ms + L * late_ms),

@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define WISE_ABI_VERSION 5
+#define WISE_ABI_VERSION 6
 
 typedef enum {
   WISE_OK = 0,
@@ -238,15 +238,17 @@ wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k,
  * wise_sparse_attn_grouped — the same late step (Section 5.2, eq.
  * "wise_attention"), bit for bit the same outputs as wise_sparse_attn, run
  * by work-groups of wise_sparse_group_rows(s) consecutive query blocks of a
- * head (4 at head_dim 128, 2 otherwise) over the union of their supports:
- * each staged key tile serves all of the group's rows that hold it, and
- * every row attends only its own blocks.  Faster than wise_sparse_attn when
- * consecutive rows' supports nearly coincide (dense supports: measured 10%
- * at density 0.91, 4.5% at 0.95), slower when they differ (30% slower at
- * density 0.43); the caller picks, e.g. by the support's density.  Where
- * grouping is unavailable (block != 64, more than 1024 key blocks, or
- * seq_len not a multiple of 128; wise_sparse_group_rows(s) == 0) the call
- * runs wise_sparse_attn's kernel.  Arguments as wise_sparse_attn, without
+ * head (block 64: 4 at head_dim 128, 2 otherwise; block 128: 2 at head_dim
+ * 128) over the union of their supports: each staged key tile serves all of
+ * the group's rows that hold it, and every row attends only its own blocks.
+ * Faster than wise_sparse_attn when consecutive rows' supports nearly
+ * coincide (dense supports: measured 10% at density 0.91, 4.5% at 0.95),
+ * slower when they differ (30% slower at density 0.43); the caller picks,
+ * e.g. by the support's density.  Where grouping is unavailable (block 16
+ * or 32, block 128 below head_dim 128, more than 1024 key blocks, or
+ * seq_len not a multiple of the group's queries: 256 at head_dim 128, else
+ * 128; wise_sparse_group_rows(s) == 0) the call runs wise_sparse_attn's
+ * kernel.  Arguments as wise_sparse_attn, without
  * row_order (groups are issued heaviest first, per head).
  * Errors: WISE_ERR_NULL, WISE_ERR_SHAPE, WISE_ERR_UNSUPPORTED, WISE_ERR_HIP.
  */

@@ -552,20 +552,22 @@ sparse_attn_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Block-sparse attention for 64-key blocks over groups of consecutive rows:
-// the dense kernel's work-group (NW waves, 32 NW queries: 4 rows at head_dim
-// 128, 2 otherwise) walks the ascending union of its rows' supports in
-// 64-key tiles, staging each tile once for all its waves, and each wave
-// attends only the tiles its own row holds (its diagonal block masked), so
-// every row gets exactly its own attention.  Where consecutive rows' supports
-// nearly coincide (dense supports) the union adds few tiles and every staged
-// tile feeds 2-4 times the queries of the one-row group; where they differ,
-// the union walk costs more than it saves.  The membership of each row and
-// the union are built in LDS as bitmasks (up to 1024 key blocks).
+// Block-sparse attention over groups of consecutive rows of BR-key blocks:
+// the dense kernel's work-group (NW waves, 32 NW queries: 4 rows of 64 or 2
+// of 128 keys at head_dim 128, 2 rows of 64 otherwise) walks the ascending
+// union of its rows' supports in 64-key tiles, staging each tile once for all
+// its waves, and each wave attends only the tiles its own row holds (its
+// diagonal block masked, tiles wholly past its queries skipped), so every row
+// gets exactly its own attention, in the one-row kernel's tile order.  Where
+// consecutive rows' supports nearly coincide (dense supports) the union adds
+// few tiles and every staged tile feeds 2-4 times the queries of the one-row
+// group; where they differ, the union walk costs more than it saves.  The
+// membership of each row and the union are built in LDS as bitmasks (up to
+// 1024 key blocks).
 // ---------------------------------------------------------------------------
 constexpr int kGroupMaskWords = 16;
 
-template <int D, int NW>
+template <int D, int NW, int BR>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                     const uint16_t* __restrict__ V, const int32_t* __restrict__ row_ptr,
@@ -573,7 +575,9 @@ sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
                     float* __restrict__ lse, int n, int nb, int heads, int gq, Sched sc,
                     float c) {
   using G = Geo<D>;
-  constexpr int kNT = NW * 64, kQT = NW * 32, kR = kQT / kKeyTile;   // rows per group
+  constexpr int kNT = NW * 64, kQT = NW * 32, kR = kQT / BR;   // rows per group
+  constexpr int kTPB = BR / kKeyTile, kWR = BR / 32;           // tiles per block, waves per row
+  static_assert(kR >= 2 && kQT % BR == 0 && BR % kKeyTile == 0, "group of rows");
   constexpr int kW = kGroupMaskWords;
   constexpr int kBufs = NW == 8 ? 2 : 1;
   __shared__ __attribute__((aligned(16))) uint16_t ks[kBufs * G::kKElems];
@@ -585,7 +589,7 @@ sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
   const int qt = sc.items - 1 - item;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qbase = qt * kQT, q0 = qbase + 32 * wave;
-  const int qb0 = qt * kR, mine = wave >> 1;      // the group's first row; this wave's row
+  const int qb0 = qt * kR, mine = wave / kWR;     // the group's first row; this wave's row
   const size_t hoff = (size_t)bh * n * D;
   const size_t kvoff = (size_t)kv_head(bh, heads, gq) * n * D;
   const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(K + kvoff), rv = buffer_rsrc(V + kvoff);
@@ -593,72 +597,107 @@ sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
 
   WaveRows<D> w;
   w.load_q(Q + hoff, q0, lane);
+  // The group's first tile is its union's lowest block: block 0 wherever a
+  // row holds the sink block, so that tile's loads start before the
+  // supports are read (and are reissued for another first block).
+  TileStage<D, kNT, true> st;
+  st.load(rk, rv, 0, tid);
   w.reset();
+  // The group's rows are consecutive CSR rows: their entries form one range,
+  // read in one pass.
+  const int row0 = bh * nb + qb0;
+  int bound[kR + 1];
+#pragma unroll
+  for (int r = 0; r <= kR; ++r) bound[r] = row_ptr[row0 + r];
   for (int i = tid; i < (kR + 1) * kW; i += kNT) {
     if (i < kR * kW) rmask[i / kW][i % kW] = 0ull;
     else umask[i - kR * kW] = 0ull;
   }
   __syncthreads();
   // Valid ids (0..qb) of every row of the group into the bitmasks.
+  for (int e = bound[0] + tid; e < bound[kR]; e += kNT) {
+    const int kb = col_idx[e];
+    int r = 0;
 #pragma unroll
-  for (int r = 0; r < kR; ++r) {
-    const int row = bh * nb + qb0 + r, qb = qb0 + r;
-    const int beg = row_ptr[row], end = row_ptr[row + 1];
-    for (int e = beg + tid; e < end; e += kNT) {
-      const int kb = col_idx[e];
-      if ((unsigned)kb <= (unsigned)qb) {
-        const unsigned long long bit = 1ull << (kb & 63);
-        atomicOr(&rmask[r][kb >> 6], bit);
-        atomicOr(&umask[kb >> 6], bit);
-      }
+    for (int j = 1; j < kR; ++j) r += e >= bound[j];
+    if ((unsigned)kb <= (unsigned)(qb0 + r)) {
+      const unsigned long long bit = 1ull << (kb & 63);
+      atomicOr(&rmask[r][kb >> 6], bit);
+      atomicOr(&umask[kb >> 6], bit);
     }
   }
   __syncthreads();
-  // Ascending set bits of the union (the same sequence in every wave).
-  int wi = 0;
-  unsigned long long cur = words > 0 ? umask[0] : 0ull;
-  auto next = [&](int& kb) {
+  // The 64-key tiles of the union's blocks in ascending order (the same
+  // sequence in every wave; block cb's tiles are cb * kTPB + 0 .. kTPB - 1),
+  // each with this wave's membership.  The walk holds the union's and its
+  // row's current 64-block words as wave-uniform values and reads LDS only
+  // when it moves on to the next word, so no tile waits on an LDS read for
+  // its membership between the barrier and its MFMAs.
+  auto uniform64 = [](unsigned long long x) {
+    const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)x);
+    const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(x >> 32));
+    return ((unsigned long long)hi << 32) | lo;
+  };
+  int wi = 0, cb = 0, sub = kTPB - 1;
+  unsigned long long cur = uniform64(umask[0]), mw = uniform64(rmask[mine][0]);
+  bool cm = false;                                  // this wave's row holds block cb
+  auto next = [&](int& tile, bool& mem) {
+    if (sub + 1 < kTPB) {
+      tile = cb * kTPB + ++sub;
+      mem = cm;
+      return true;
+    }
     while (cur == 0ull) {
       if (++wi >= words) return false;
-      cur = umask[wi];
+      cur = uniform64(umask[wi]);
+      mw = uniform64(rmask[mine][wi]);
     }
-    kb = (wi << 6) + __builtin_ctzll(cur);
+    const int bit = __builtin_ctzll(cur);
+    cb = (wi << 6) + bit;
     cur &= cur - 1ull;
+    cm = (mw >> bit) & 1ull;
+    sub = 0;
+    tile = cb * kTPB;
+    mem = cm;
     return true;
   };
-  auto member = [&](int kb) { return (rmask[mine][kb >> 6] >> (kb & 63)) & 1ull; };
-  auto attend = [&](const uint16_t* kt, const uint16_t* vv, int kb) {
-    if (!member(kb)) return;
-    if (kb * kKeyTile + kKeyTile - 1 > q0) w.template attend<true>(kt, vv, lane, c, kb * kKeyTile, q0);
-    else w.template attend<false>(kt, vv, lane, c, kb * kKeyTile, q0);
+  // One instance of the tile step for every tile (it masks only a tile that
+  // reaches past the wave's first query): a second, unmasked instance for
+  // the tiles below the diagonal costs registers and code for nothing.
+  auto attend = [&](const uint16_t* kt, const uint16_t* vv, int tile, bool mem) {
+    const int key0 = tile * kKeyTile;
+    if (!mem || key0 > q0) return;
+    w.template attend<true>(kt, vv, lane, c, key0, q0);
   };
 
-  TileStage<D, kNT, true> st;
-  int kb = 0, kb1 = 0, kb2 = 0;
-  bool have = next(kb);
-  if (have) st.load(rk, rv, kb * kKeyTile, tid);
+  int kb = 0, kb1 = 0, kb2 = 0;     // tiles: current, next, the one after
+  bool m0 = false, m1 = false, m2 = false;
+  bool have = next(kb, m0);
+  if (have && kb != 0) st.load(rk, rv, kb * kKeyTile, tid);
   if constexpr (kBufs == 2) {
     // Double-buffered as the dense 8-wave group: tile i+1 is stored into the
     // idle buffer right after tile i is computed, one barrier per tile.
     if (have) {
       st.store(ks, vt, tid);
-      bool h1 = next(kb1);
+      bool h1 = next(kb1, m1);
       if (h1) st.load(rk, rv, kb1 * kKeyTile, tid);
       __syncthreads();
       for (int it = 0;; ++it) {
         const int cu = it & 1;
-        attend(ks + cu * G::kKElems, vt + cu * G::kVElems, kb);
+        attend(ks + cu * G::kKElems, vt + cu * G::kVElems, kb, m0);
         bool h2 = false;
         if (h1) {
           const int nx = (it + 1) & 1;
           st.store(ks + nx * G::kKElems, vt + nx * G::kVElems, tid);
-          h2 = next(kb2);
+          h2 = next(kb2, m2);
           if (h2) st.load(rk, rv, kb2 * kKeyTile, tid);
         }
         __syncthreads();
         if (!h1) break;
         kb = kb1;
+        m0 = m1;
         kb1 = kb2;
+        m1 = m2;
         h1 = h2;
       }
     }
@@ -666,11 +705,12 @@ sparse_group_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     while (have) {
       st.store(ks, vt, tid);
       __syncthreads();
-      const bool more = next(kb1);
+      const bool more = next(kb1, m1);
       if (more) st.load(rk, rv, kb1 * kKeyTile, tid);
-      attend(ks, vt, kb);
+      attend(ks, vt, kb, m0);
       __syncthreads();
       kb = kb1;
+      m0 = m1;
       have = more;
     }
   }
@@ -878,27 +918,32 @@ static hipError_t launch_sparse_d(const Dims& s, const void* q, const void* k, c
   return hipGetLastError();
 }
 
-template <int D, int NW>
+template <int D, int NW, int BR = 64>
 static void launch_group_nw(const Dims& s, const void* q, const void* k, const void* v,
                             const int32_t* rp, const int32_t* ci, void* o, float* lse,
                             hipStream_t st) {
   const Sched sc = make_sched(s.bh, s.n / (NW * 32), (size_t)s.n * D * 4 / s.gq);
-  hipLaunchKernelGGL((sparse_group_kernel<D, NW>), dim3(sched_grid(sc)), dim3(NW * 64), 0, st,
+  hipLaunchKernelGGL((sparse_group_kernel<D, NW, BR>), dim3(sched_grid(sc)), dim3(NW * 64), 0, st,
                      (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, rp, ci,
                      (uint16_t*)o, lse, s.n, s.nb, s.heads, s.gq, sc, s.scale * kLog2e);
 }
 
 int sparse_group_rows(const Dims& s) {
-  if (s.block != 64 || s.nb > 64 * kGroupMaskWords) return 0;
+  if (s.nb > 64 * kGroupMaskWords) return 0;
   const int qt = dense_query_tile(s);
-  return qt >= 128 ? qt / 64 : 0;
+  if (s.block == 64) return qt >= 128 ? qt / 64 : 0;
+  if (s.block == 128) return qt == 256 ? 2 : 0;
+  return 0;
 }
 
 hipError_t launch_sparse_grouped(const Dims& s, const void* q, const void* k, const void* v,
                                  const int32_t* rp, const int32_t* ci, void* o, float* lse,
                                  hipStream_t st) {
   const int rows = sparse_group_rows(s);
-  if (rows == 4 && s.d == 128) launch_group_nw<128, 8>(s, q, k, v, rp, ci, o, lse, st);
+  if (s.block == 128) {
+    if (rows == 2 && s.d == 128) launch_group_nw<128, 8, 128>(s, q, k, v, rp, ci, o, lse, st);
+    else return launch_sparse(s, q, k, v, rp, ci, nullptr, o, lse, st);
+  } else if (rows == 4 && s.d == 128) launch_group_nw<128, 8>(s, q, k, v, rp, ci, o, lse, st);
   else if (rows == 2 && s.d == 128) launch_group_nw<128, 4>(s, q, k, v, rp, ci, o, lse, st);
   else if (rows == 2 && s.d == 96) launch_group_nw<96, 4>(s, q, k, v, rp, ci, o, lse, st);
   else if (rows == 2 && s.d == 64) launch_group_nw<64, 4>(s, q, k, v, rp, ci, o, lse, st);

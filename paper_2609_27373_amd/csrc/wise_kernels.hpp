@@ -24,9 +24,10 @@ int dense_query_tile(const Dims& s);   // queries per dense work-group: 64, 128 
 hipError_t launch_sparse(const Dims& s, const void* q, const void* k, const void* v,
                          const int32_t* row_ptr, const int32_t* col_idx, const int32_t* order,
                          void* o, float* lse, hipStream_t st);
-// Block 64: work-groups of 2 or 4 consecutive rows over the union of their
-// supports (sparse_group_rows(s) rows per group; 0: not available, and
-// launch_sparse_grouped runs launch_sparse instead).
+// Blocks of 64 keys (groups of 4 rows at head_dim 128, else 2) and of 128
+// keys at head_dim 128 (groups of 2 rows): work-groups of consecutive rows
+// over the union of their supports (sparse_group_rows(s) rows per group; 0:
+// not available, and launch_sparse_grouped runs launch_sparse instead).
 int sparse_group_rows(const Dims& s);
 hipError_t launch_sparse_grouped(const Dims& s, const void* q, const void* k, const void* v,
                                  const int32_t* row_ptr, const int32_t* col_idx, void* o,

@@ -20,14 +20,15 @@ Two late-step kernels compute the same outputs (late_kernel):
              the union of their supports (faster where supports are dense)
   "auto"     grouped where the library offers it and the selected support's
              density (nnz over the causal block pairs) is at least
-             group_density, rows otherwise.  The first select() reads nnz
-             back (one synchronisation); later ones copy it to pinned host
-             memory asynchronously, and the choice follows when the copy
-             has landed (checked without waiting at each select() and late
-             step), so the host never waits on the device again.  Both
-             kernels give the same outputs, so when the switch happens does
-             not change any result.  A select() under graph capture keeps
-             the current choice.
+             group_density (by default the measured break-even of the
+             library's group shape, GROUP_DENSITY), rows otherwise.  The
+             first select() reads nnz back (one synchronisation); later ones
+             copy it to pinned host memory asynchronously, and the choice
+             follows when the copy has landed (checked without waiting at
+             each select() and late step), so the host never waits on the
+             device again.  Both kernels give the same outputs, so when the
+             switch happens does not change any result.  A select() under
+             graph capture keeps the current choice.
 
 Buffers are allocated once per trajectory (torch device memory); every call
 enqueues on the current stream and returns (except the first select() in
@@ -44,15 +45,20 @@ from . import wise
 class WisePipeline:
     MODES = ("accumulate", "union")
     LATE_KERNELS = ("auto", "rows", "grouped")
-    # Density from which "auto" picks the grouped kernel: measured at 4K,
-    # 32 heads, d 128, block 64 it runs 10% faster at density 0.91 and 30%
-    # slower at 0.43; the union of consecutive rows' supports grows about as
-    # fast as the density falls, and the break-even lies near 0.85.
-    GROUP_DENSITY = 0.85
+    # Density from which "auto" picks the grouped kernel, by (block, rows per
+    # group).  The union of consecutive rows' supports grows as the density
+    # falls, and the break-even is where it costs what the shared staging
+    # saves.  Late step, grouped over one-row time on the same supports:
+    #   block 64, 4 rows (d 128): 1.36 at density 0.39, 1.18 at 0.58, 1.08 at
+    #     0.69, 1.04 at 0.74, 0.95 at 0.80, 0.94 at 0.88, 0.88 at 0.91
+    #   block 64, 2 rows (d 96): 0.98 at 0.54, 0.94 at 0.78, 0.90 at 0.89-0.95
+    #   block 128, 2 rows (d 128): 1.01 at 0.70, 1.00 at 0.80, 0.97 at 0.91,
+    #     0.97 at 0.96
+    GROUP_DENSITY = {(64, 4): 0.78, (64, 2): 0.55, (128, 2): 0.80}
 
     def __init__(self, batch, heads, seq_len, head_dim, block, tau, flags=wise.WISE_DEFAULT_FLAGS,
                  scale=0.0, device="cuda", mode="accumulate", window=4, kv_heads=0,
-                 late_kernel="auto", group_density=GROUP_DENSITY):
+                 late_kernel="auto", group_density=None):
         if mode not in self.MODES:
             raise ValueError(f"mode must be one of {self.MODES}")
         if late_kernel not in self.LATE_KERNELS:
@@ -75,9 +81,12 @@ class WisePipeline:
                                      device=device)
         self.filled = 0
         self.late_kernel = late_kernel
+        group_rows = wise.wise_sparse_group_rows(self.shape)
+        if group_density is None:
+            group_density = self.GROUP_DENSITY.get((block, group_rows), 1.0)
         self.group_density = float(group_density)
         self.grouped = late_kernel == "grouped"
-        self._auto = (late_kernel == "auto" and wise.wise_sparse_group_rows(self.shape) > 0)
+        self._auto = late_kernel == "auto" and group_rows > 0
         self._decided = False
         self._nnz_host = torch.empty(1, dtype=torch.int32, pin_memory=True) if self._auto else None
         self._nnz_event = None

@@ -43,7 +43,7 @@ def test_exports(lib):
 
 
 def test_version_and_strings(lib):
-    assert wise.wise_abi_version() == 5
+    assert wise.wise_abi_version() == 6
     for st, name in wise.STATUS_NAMES.items():
         assert wise.wise_status_string(st).startswith(name)
     assert "unknown" in wise.wise_status_string(99)
@@ -150,7 +150,12 @@ def test_sparse_group_rows(lib):
     assert wise.wise_sparse_group_rows(S(head_dim=96)) == 2
     assert wise.wise_sparse_group_rows(S(head_dim=64, seq_len=320)) == 0     # 64-query tiles
     assert wise.wise_sparse_group_rows(S(block=32)) == 0
-    assert wise.wise_sparse_group_rows(S(block=128)) == 0
+    assert wise.wise_sparse_group_rows(S(block=128)) == 0                    # 128-key rows: d 128 only
+    assert wise.wise_sparse_group_rows(S(block=128, head_dim=96)) == 0
+    assert wise.wise_sparse_group_rows(S(block=128, head_dim=128)) == 2      # two rows of 4 waves
+    assert wise.wise_sparse_group_rows(S(block=128, head_dim=128, seq_len=640)) == 0
+    assert wise.wise_sparse_group_rows(S(block=128, head_dim=128, seq_len=128 * 1024)) == 2
+    assert wise.wise_sparse_group_rows(S(block=128, head_dim=128, seq_len=128 * 1026)) == 0
     assert wise.wise_sparse_group_rows(S(seq_len=64 * 2048)) == 0            # > 1024 key blocks
     assert wise.wise_sparse_group_rows(S(seq_len=500)) == -1
 

@@ -162,13 +162,17 @@ def test_full_support_sparse_equals_dense(gpu_lib, d, B):
 @pytest.mark.parametrize("bt,h,kvh,n,d,B", [
     (1, 2, 2, 1024, 128, 64), (2, 3, 3, 640, 128, 64), (1, 4, 2, 512, 96, 64), (2, 2, 1, 384, 64, 64),
     (1, 2, 2, 512, 96, 32), (1, 2, 2, 512, 128, 128), (1, 2, 2, 320, 64, 64),
+    (2, 3, 3, 1280, 128, 128), (1, 4, 2, 1024, 128, 128), (1, 2, 2, 640, 128, 128),
+    (1, 2, 2, 512, 96, 128),
 ])
 def test_grouped_equals_rows(gpu_lib, bt, h, kvh, n, d, B):
-    """wise_sparse_attn_grouped (block 64: 4 or 2 consecutive rows per group
-    over the union of their supports) gives wise_sparse_attn's outputs bit
-    for bit, and both match the oracle: random rows, empty rows, local bands,
-    full rows, rows without their diagonal block and ids past the diagonal.
-    Other blocks, and 64-query tiles (n = 320), run the one-row kernel."""
+    """wise_sparse_attn_grouped (block 64: 4 or 2 consecutive rows per group,
+    block 128 at d 128: 2, over the union of their supports) gives
+    wise_sparse_attn's outputs bit for bit, and both match the oracle: random
+    rows, empty rows, local bands, full rows, rows without their diagonal
+    block and ids past the diagonal.  Block 32, block 128 below d 128 and
+    lengths the group's queries do not divide (n = 320 at d 64, 640 at d 128
+    with block 128) run the one-row kernel."""
     w = gpu_lib
     nb = n // B
     s = w.make_shape(bt, h, n, d, B, kv_heads=kvh)
