@@ -55,16 +55,16 @@ PEAK_HBM_GBS = 8000.0
 # for one plain 256 MiB device copy (fetch x2, write x1), and the trace's
 # average kernel duration.  They hold only for the kernel sources they were
 # taken on (MEASURED_DIGEST); any other digest reports null.
-MEASURED_DIGEST = "7b5ff3d443b6ba80"
+MEASURED_DIGEST = "f23d2ef9210f708e"
 MEASURED = {
-    "4k": {"bytes": 193906886, "rocprof_avg_ms": 0.15474},
-    "4k-pr": {"bytes": 249071847, "rocprof_avg_ms": 0.09529},
-    "4k-b32": {"bytes": 941281634, "rocprof_avg_ms": 0.53538},
-    "4k-b16": {"bytes": 763097722, "rocprof_avg_ms": 0.87781},
-    "4k-gqa": {"bytes": 905818382, "rocprof_avg_ms": 0.29075},
-    "8k": {"bytes": 363896338, "rocprof_avg_ms": 0.86717},
-    "16k": {"bytes": 3733876052, "rocprof_avg_ms": 4.32854},
-    "32k": {"bytes": 5186282415, "rocprof_avg_ms": 8.13629},
+    "4k": {"bytes": 195237728, "rocprof_avg_ms": 0.15448},
+    "4k-pr": {"bytes": 248294269, "rocprof_avg_ms": 0.09523},
+    "4k-b32": {"bytes": 942413857, "rocprof_avg_ms": 0.54182},
+    "4k-b16": {"bytes": 763101281, "rocprof_avg_ms": 0.88011},
+    "4k-gqa": {"bytes": 910790193, "rocprof_avg_ms": 0.29545},
+    "8k": {"bytes": 378601560, "rocprof_avg_ms": 0.82118},
+    "16k": {"bytes": 2007145419, "rocprof_avg_ms": 4.20584},
+    "32k": {"bytes": 3978352404, "rocprof_avg_ms": 8.00235},
 }
 KERNEL_SOURCES = ("attention.hip", "wise_device.hpp")
 
