@@ -205,6 +205,15 @@ def test_fullsize_trajectory(gpu_lib, name):
     assert_attn(f64(o2.view(-1, n, d).index_select(0, idx)), o_sref,
                 f"late step O (oracle CSR), {len(sel) * nb} rows")
     assert_lse(f64(l2.view(-1, n).index_select(0, idx)), l_sref, "late step lse (oracle CSR)")
+    if w.wise_sparse_group_rows(pipe.shape) > 0:
+        # the grouped late step on the same CSR: the one-row kernel's bits, every row of the shape
+        o3, l3 = torch.empty_like(out), torch.empty_like(lse)
+        w.wise_sparse_attn_grouped(pipe.shape, q, k, v, torch.from_numpy(rp_o).cuda(),
+                                   torch.from_numpy(ci_o).cuda(), o3, l3)
+        torch.cuda.synchronize()
+        assert torch.equal(o2, o3) and torch.equal(l2, l3)
+        say(f"{name}: grouped late step ({w.wise_sparse_group_rows(pipe.shape)} rows per group, "
+            f"pipeline {'grouped' if pipe.grouped else 'one-row'}) bitwise equal to the one-row kernel")
 
     # 6. selection only, every row of the full shape
     acc_host = synthetic_masses((cfg.batch, cfg.heads, nb, nb), seed=cfg.seed + 101,

@@ -367,6 +367,13 @@ def test_union_fullsize(gpu_lib, name):
     ref = orc.sparse(td + 1, oracle_rows)
     assert_attn(f64(o2.view(-1, n, d).index_select(0, idx)),
                 np.stack([ref[s][0] for s in sel]), "union late step O (oracle CSR)")
+    if w.wise_sparse_group_rows(pipe.shape) > 0:
+        o3 = torch.empty_like(out)
+        w.wise_sparse_attn_grouped(pipe.shape, q, k, v, torch.from_numpy(rp_o).cuda(),
+                                   torch.from_numpy(ci_o).cuda(), o3, None)
+        torch.cuda.synchronize()
+        assert torch.equal(o2, o3)
+        say(f"  grouped late step on the union CSR bitwise equal to the one-row kernel")
     dens = rp[-1] / (bh * nb * (nb + 1) / 2)
     say(f"  union density {dens:.4f}, retained future mass (step t_d+1) {frac:.4f}")
     assert 0.0 < frac <= 1.0 + 1e-9 and frac >= 0.9 * cfg.tau
