@@ -160,6 +160,23 @@ def test_sparse_group_rows(lib):
     assert wise.wise_sparse_group_rows(S(seq_len=500)) == -1
 
 
+def test_group_density_covers_every_group_shape(lib):
+    """The pipeline's automatic late-kernel choice has a measured break-even
+    density for every group shape the library can return."""
+    from paper_2609_27373_amd.pipeline import WisePipeline
+    seen = set()
+    for d in (64, 96, 128):
+        for block in (16, 32, 64, 128):
+            for n in (128, 256, 384, 512, 640, 4096, 8192, 65536, 131072):
+                if n % block:
+                    continue
+                rows = wise.wise_sparse_group_rows(S(head_dim=d, block=block, seq_len=n))
+                if rows > 0:
+                    seen.add((block, rows))
+                    assert (block, rows) in WisePipeline.GROUP_DENSITY, (d, block, n, rows)
+    assert seen == set(WisePipeline.GROUP_DENSITY)
+
+
 MIS8 = ctypes.c_void_p(4096 + 4)    # 4-byte but not 8-byte aligned
 
 
