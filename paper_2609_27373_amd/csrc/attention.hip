@@ -5,8 +5,10 @@
 //                       optionally the block-pooled attention mass
 //                       (Section 5.1, eq. block_attention_mass)
 //   sparse_attn_kernel  attention restricted to a CSR block support
-//   sparse_row16_kernel (Section 5.2, eq. wise_attention); the second for
-//                       16-key blocks
+//   sparse_group_kernel (Section 5.2, eq. wise_attention): one work-group
+//   sparse_row16_kernel per row; groups of consecutive rows over the union
+//                       of their supports (the same outputs, for dense
+//                       supports); one wave per row of 16-key blocks
 //
 // Shared tile engine.  A wave owns 32 consecutive queries.  For each tile of
 // 64 keys (32 for 32-key blocks) it computes S^T = K Q^T with
