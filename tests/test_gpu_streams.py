@@ -47,11 +47,12 @@ def test_two_streams_match_sequential(gpu_lib):
     assert torch.equal(seq[0], par[0]) and torch.equal(seq[1], par[1])
 
 
-def test_graph_replays_match_eager(gpu_lib):
+@pytest.mark.parametrize("late_kernel", ["rows", "grouped"])
+def test_graph_replays_match_eager(gpu_lib, late_kernel):
     cfg = CONFIGS["tiny"].with_(heads=4, seq_len=1024)
-    say(f"graph capture: heads {cfg.heads} n {cfg.seq_len}")
+    say(f"graph capture: heads {cfg.heads} n {cfg.seq_len}, late kernel {late_kernel}")
     steps = _trajectory_inputs(cfg, cfg.discovery_steps + 1)
-    pipe = WisePipeline.for_config(cfg)
+    pipe = WisePipeline.for_config(cfg, late_kernel=late_kernel)
     out = torch.empty_like(steps[0][0])
     pipe.reset()
     for t in range(1, cfg.discovery_steps + 1):
@@ -93,13 +94,14 @@ def test_graph_replays_match_eager(gpu_lib):
     assert torch.equal(pipe.acc, acc_eager)
 
 
-def test_captured_late_step_follows_new_inputs_and_supports(gpu_lib):
+@pytest.mark.parametrize("late_kernel", ["rows", "grouped"])
+def test_captured_late_step_follows_new_inputs_and_supports(gpu_lib, late_kernel):
     """LateStepGraph: replays after writing new Q/K/V into the captured
     buffers, and after a new selection, give the eager late step's bits."""
     cfg = CONFIGS["tiny"].with_(heads=4, seq_len=1024)
-    say(f"late-step graph: heads {cfg.heads} n {cfg.seq_len}")
+    say(f"late-step graph: heads {cfg.heads} n {cfg.seq_len}, late kernel {late_kernel}")
     steps = _trajectory_inputs(cfg, cfg.discovery_steps + 3)
-    pipe = WisePipeline.for_config(cfg)
+    pipe = WisePipeline.for_config(cfg, late_kernel=late_kernel)
     out = torch.empty_like(steps[0][0])
     pipe.reset()
     for t in range(1, cfg.discovery_steps + 1):
