@@ -1,6 +1,7 @@
 """Seeded random geometries through the whole path on the GPU: dense
 attention with mass pooling, selection, and the late step on the selected
-support, each against the oracle on the same bf16 inputs.  Every draw stays
+support, each against the oracle on the same bf16 inputs (the grouped late
+step bit for bit against the one-row kernel).  Every draw stays
 inside the documented limits (head_dim 64/96/128, block 16/32/64/128,
 seq_len a multiple of the block and of 64, heads a multiple of kv_heads)."""
 
@@ -85,6 +86,14 @@ def test_random_geometry_end_to_end(gpu_lib, seed):
     torch.cuda.synchronize()
     assert_attn(o2, o_ref2, "sparse O (oracle CSR)")
     assert_lse(l2, l_ref2, "sparse lse (oracle CSR)")
+    # the grouped late step on the same support: the same bits (it runs the
+    # one-row kernel where the shape has no group)
+    o3 = torch.empty_like(qd)
+    l3 = torch.empty((bt, h, n), device="cuda")
+    w.wise_sparse_attn_grouped(s, qd, kd, vd, torch.from_numpy(rp_ref).cuda(),
+                               torch.from_numpy(ci_ref).cuda(), o3, l3)
+    torch.cuda.synchronize()
+    assert torch.equal(o2, o3) and torch.equal(l2, l3), "grouped late step"
     # and on the GPU's own support, on the rows whose supports agree
     w.wise_sparse_attn(s, qd, kd, vd, sched.row_ptr, sched.col_idx, sched.row_order, o2, l2)
     torch.cuda.synchronize()
