@@ -337,9 +337,17 @@ def cpu_baseline(cfg, min_s=10.0, max_late=8):
     # minutes; take the oracle selection on the window masses of ONE head,
     # reused for every sampled head (same shape and planted structure).
     f = lambda x: x.float().numpy().astype(np.float64)  # noqa: E731
+    t0 = time.perf_counter()
     masses = [O.block_mass(f(disc[t - 1][0][:, :1]), f(disc[t - 1][1][:, :1]), cfg.block)
               for t in cfg.window]
+    t_mass = (time.perf_counter() - t0) / len(cfg.window)
+    t0 = time.perf_counter()
+    qd, kd, vd = (f(x[:, :1]) for x in disc[-1])
+    O.dense_attention(qd, kd, vd)
+    t_dense = time.perf_counter() - t0
+    t0 = time.perf_counter()
     rp1, ci1 = O.select_support(O.accumulate(masses).astype(np.float32), float(np.float32(cfg.tau)))
+    t_sel = time.perf_counter() - t0
     per_head = metrics.effective_flops(rp1, ci1, cfg.nb, cfg.block, cfg.head_dim)
     del disc
     flops = heads = steps = 0
@@ -359,8 +367,15 @@ def cpu_baseline(cfg, min_s=10.0, max_late=8):
         dt += time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()
                    if p.get("user_api") == "blas"] or [1])
+    nh = cfg.batch * cfg.heads
+    # The oracle's whole step, per phase: head 0 timed, times the head count.
+    phases = {"dense_step": t_dense * nh, "dense_plus_mass_step": (t_dense + t_mass) * nh,
+              "selection": t_sel * nh, "late_step": dt / heads * nh}
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
+            "seconds_per_step": {k: round(v, 3) for k, v in phases.items()},
+            "seconds_per_step_note": f"one head timed per phase (late step: the sample's mean per head), "
+                                     f"times {nh} heads",
             "sample": f"numpy fp64 sparse attention (gather form) of the {cfg.name} workload: "
                       f"{heads} (step, head) pairs over {steps} late steps of {cfg.batch * cfg.heads} "
                       f"heads each, {dt:.1f} s timed, support of head 0 (oracle selection) reused; "
