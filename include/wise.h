@@ -242,9 +242,10 @@ wise_status wise_sparse_attn(const wise_shape* s, const void* q, const void* k,
  * 128) over the union of their supports: each staged key tile serves all of
  * the group's rows that hold it, and every row attends only its own blocks.
  * Faster than wise_sparse_attn when consecutive rows' supports nearly
- * coincide (dense supports: measured 10% at density 0.91, 4.5% at 0.95),
- * slower when they differ (30% slower at density 0.43); the caller picks,
- * e.g. by the support's density.  Where grouping is unavailable (block 16
+ * coincide (dense supports: measured 12% at density 0.91 with 4 rows of 64
+ * keys, 10% at 0.95 with 2 rows), slower when they differ (27% slower at
+ * density 0.43 with 4 rows); the caller picks, e.g. by the support's
+ * density against the break-even of the group shape.  Where grouping is unavailable (block 16
  * or 32, block 128 below head_dim 128, more than 1024 key blocks, or
  * seq_len not a multiple of the group's queries: 256 at head_dim 128, else
  * 128; wise_sparse_group_rows(s) == 0) the call runs wise_sparse_attn's
