@@ -219,6 +219,43 @@ def test_grouped_equals_rows(gpu_lib, bt, h, kvh, n, d, B):
     assert_lse(l_g, l_ref, "grouped lse")
 
 
+@pytest.mark.parametrize("n,B", [(65536, 64), (131072, 128)])
+def test_grouped_at_most_key_blocks(gpu_lib, n, B):
+    """1024 key blocks, the grouped kernel's largest support (16 mask words
+    per row): sparse random rows with the sink, a block in every 64-block word
+    and the diagonal give the one-row kernel's bits, and the oracle's values."""
+    w = gpu_lib
+    d, nb = 128, n // B
+    s = w.make_shape(1, 1, n, d, B)
+    assert w.wise_sparse_group_rows(s) > 0
+    say(f"grouped at {nb} key blocks: n={n} B={B}, {w.wise_sparse_group_rows(s)} rows per group")
+    g = torch.Generator().manual_seed(n + B)
+    q = (torch.randn((1, 1, n, d), generator=g) * 1.5).to(torch.bfloat16).cuda()
+    k = torch.randn((1, 1, n, d), generator=g).to(torch.bfloat16).cuda()
+    v = torch.randn((1, 1, n, d), generator=g).to(torch.bfloat16).cuda()
+    rng = np.random.default_rng(n)
+    rp, ci = [0], []
+    for qb in range(nb):
+        ids = {0, qb} | {int(x) for x in rng.integers(0, qb + 1, size=3)}
+        ids |= {int(wd * 64 + rng.integers(64)) for wd in range(qb // 64 + 1) if wd * 64 <= qb}
+        ids = sorted(x for x in ids if x <= qb)
+        ci.extend(ids)
+        rp.append(len(ci))
+    rp_t = torch.tensor(rp, dtype=torch.int32, device="cuda")
+    ci_t = torch.tensor(ci, dtype=torch.int32, device="cuda")
+    o_r, o_g = torch.empty_like(q), torch.empty_like(q)
+    l_r, l_g = (torch.empty((1, 1, n), device="cuda") for _ in range(2))
+    w.wise_sparse_attn(s, q, k, v, rp_t, ci_t, None, o_r, l_r)
+    w.wise_sparse_attn_grouped(s, q, k, v, rp_t, ci_t, o_g, l_g)
+    torch.cuda.synchronize()
+    assert torch.equal(o_r, o_g) and torch.equal(l_r, l_g)
+    # against the oracle, every row
+    o_ref, l_ref = O.sparse_attention(f64(q), f64(k), f64(v), np.array(rp, np.int32),
+                                      np.array(ci, np.int32), B)
+    assert_attn(o_g, o_ref, f"grouped O, {nb} rows")
+    assert_lse(l_g, l_ref, "grouped lse")
+
+
 def test_sparse_edge_rows(gpu_lib):
     """Empty rows give O = 0 and lse = -inf; ids past the diagonal are skipped."""
     w = gpu_lib
