@@ -256,6 +256,30 @@ def test_grouped_at_most_key_blocks(gpu_lib, n, B):
     assert_lse(l_g, l_ref, "grouped lse")
 
 
+def test_grouped_past_1024_key_blocks_runs_the_one_row_kernel(gpu_lib):
+    """1032 key blocks: no group shape (the masks hold 1024), so the grouped
+    call runs the one-row kernel in natural row order: the same bits as
+    wise_sparse_attn without a row order."""
+    w = gpu_lib
+    n, d, B = 1032 * 64, 128, 64
+    s = w.make_shape(1, 1, n, d, B)
+    assert w.wise_sparse_group_rows(s) == 0
+    g = torch.Generator().manual_seed(5)
+    q, k, v = ((torch.randn((1, 1, n, d), generator=g)).to(torch.bfloat16).cuda() for _ in range(3))
+    nb = n // B
+    rp, ci = [0], []
+    for qb in range(nb):
+        ci.extend(sorted({0, qb, qb // 2}))
+        rp.append(len(ci))
+    rp_t = torch.tensor(rp, dtype=torch.int32, device="cuda")
+    ci_t = torch.tensor(ci, dtype=torch.int32, device="cuda")
+    o_r, o_g = torch.empty_like(q), torch.empty_like(q)
+    w.wise_sparse_attn(s, q, k, v, rp_t, ci_t, None, o_r, None)
+    w.wise_sparse_attn_grouped(s, q, k, v, rp_t, ci_t, o_g, None)
+    torch.cuda.synchronize()
+    assert torch.equal(o_r, o_g)
+
+
 def test_sparse_edge_rows(gpu_lib):
     """Empty rows give O = 0 and lse = -inf; ids past the diagonal are skipped."""
     w = gpu_lib
