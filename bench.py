@@ -18,8 +18,11 @@ rules, with the same sparse kernel on the full causal support beside the
 selected one (the paper's matched-backend comparison); the paper's
 block-size sweep at that geometry (blocks of 16, 64 and 128 keys under the
 union rule); grouped-query attention; and the 8K, 16K (threshold sweep) and
-32K workloads.  The oracle
-(CPU, fp64) is timed on a bounded sample as a baseline only.
+32K workloads.  Each leg's late steps run the kernel the pipeline picks
+from the selected support's density (one work-group per row, or groups of
+consecutive rows over the union of their supports; the same outputs), named
+in the leg's `late_kernel`.  The oracle (CPU, fp64) is timed on a bounded
+sample as a baseline only.
 
     python bench.py [--steps K] [--warmup W] [--config 4k] [--gpus 1]
 """
