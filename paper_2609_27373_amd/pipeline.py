@@ -51,10 +51,11 @@ class WisePipeline:
     # saves.  Late step, grouped over one-row time on the same supports:
     #   block 64, 4 rows (d 128): 1.36 at density 0.39, 1.18 at 0.58, 1.08 at
     #     0.69, 1.04 at 0.74, 0.95 at 0.80, 0.94 at 0.88, 0.88 at 0.91
-    #   block 64, 2 rows (d 96): 0.98 at 0.54, 0.94 at 0.78, 0.90 at 0.89-0.95
+    #   block 64, 2 rows (d 96): 1.01 at 0.30, 0.98 at 0.42 and 0.54, 1.00 at
+    #     0.55, 0.97 at 0.66, 0.94 at 0.78, 0.90 at 0.89-0.95
     #   block 128, 2 rows (d 128): 1.01 at 0.70, 1.00 at 0.80, 0.97 at 0.91,
     #     0.97 at 0.96
-    GROUP_DENSITY = {(64, 4): 0.78, (64, 2): 0.55, (128, 2): 0.80}
+    GROUP_DENSITY = {(64, 4): 0.78, (64, 2): 0.40, (128, 2): 0.80}
 
     def __init__(self, batch, heads, seq_len, head_dim, block, tau, flags=wise.WISE_DEFAULT_FLAGS,
                  scale=0.0, device="cuda", mode="accumulate", window=4, kv_heads=0,
