@@ -21,7 +21,8 @@ Two late-step kernels compute the same outputs (late_kernel):
   "auto"     grouped where the library offers it and the selected support's
              density (nnz over the causal block pairs) is at least
              group_density (by default the measured break-even of the
-             library's group shape, GROUP_DENSITY), rows otherwise.  The
+             library's group shape and head_dim, GROUP_DENSITY; some shapes
+             never), rows otherwise.  The
              first select() reads nnz back (one synchronisation); later ones
              copy it to pinned host memory asynchronously, and the choice
              follows when the copy has landed (checked without waiting at
@@ -46,16 +47,21 @@ class WisePipeline:
     MODES = ("accumulate", "union")
     LATE_KERNELS = ("auto", "rows", "grouped")
     # Density from which "auto" picks the grouped kernel, by (block, rows per
-    # group).  The union of consecutive rows' supports grows as the density
-    # falls, and the break-even is where it costs what the shared staging
-    # saves.  Late step, grouped over one-row time on the same supports:
-    #   block 64, 4 rows (d 128): 1.36 at density 0.39, 1.18 at 0.58, 1.08 at
+    # group, head_dim); None: never (slower at every density measured).  The
+    # union of consecutive rows' supports grows as the density falls, and the
+    # break-even is where it costs what the shared staging saves.  Late step,
+    # grouped over one-row time on the same supports:
+    #   block 64, 4 rows, d 128: 1.36 at density 0.39, 1.18 at 0.58, 1.08 at
     #     0.69, 1.04 at 0.74, 0.95 at 0.80, 0.94 at 0.88, 0.88 at 0.91
-    #   block 64, 2 rows (d 96): 1.01 at 0.30, 0.98 at 0.42 and 0.54, 1.00 at
+    #   block 64, 2 rows, d 128 (lengths 256 does not divide): 1.05 at 0.80,
+    #     about 1.03 at 0.91
+    #   block 64, 2 rows, d 96: 1.01 at 0.30, 0.98 at 0.42 and 0.54, 1.00 at
     #     0.55, 0.97 at 0.66, 0.94 at 0.78, 0.90 at 0.89-0.95
-    #   block 128, 2 rows (d 128): 1.01 at 0.70, 1.00 at 0.80, 0.97 at 0.91,
+    #   block 64, 2 rows, d 64: 1.07 at 0.23, 1.02 at 0.58, 0.92 at 0.89
+    #   block 128, 2 rows, d 128: 1.01 at 0.70, 1.00 at 0.80, 0.97 at 0.91,
     #     0.97 at 0.96
-    GROUP_DENSITY = {(64, 4): 0.78, (64, 2): 0.40, (128, 2): 0.80}
+    GROUP_DENSITY = {(64, 4, 128): 0.78, (64, 2, 128): None, (64, 2, 96): 0.40,
+                     (64, 2, 64): 0.70, (128, 2, 128): 0.80}
 
     def __init__(self, batch, heads, seq_len, head_dim, block, tau, flags=wise.WISE_DEFAULT_FLAGS,
                  scale=0.0, device="cuda", mode="accumulate", window=4, kv_heads=0,
@@ -84,10 +90,10 @@ class WisePipeline:
         self.late_kernel = late_kernel
         group_rows = wise.wise_sparse_group_rows(self.shape)
         if group_density is None:
-            group_density = self.GROUP_DENSITY.get((block, group_rows), 1.0)
-        self.group_density = float(group_density)
+            group_density = self.GROUP_DENSITY.get((block, group_rows, head_dim))
+        self.group_density = None if group_density is None else float(group_density)
         self.grouped = late_kernel == "grouped"
-        self._auto = late_kernel == "auto" and group_rows > 0
+        self._auto = late_kernel == "auto" and group_rows > 0 and self.group_density is not None
         self._decided = False
         self._nnz_host = torch.empty(1, dtype=torch.int32, pin_memory=True) if self._auto else None
         self._nnz_event = None

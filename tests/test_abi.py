@@ -162,7 +162,8 @@ def test_sparse_group_rows(lib):
 
 def test_group_density_covers_every_group_shape(lib):
     """The pipeline's automatic late-kernel choice has a measured break-even
-    density for every group shape the library can return."""
+    density (or a measured "never") for every group shape and head_dim the
+    library can return."""
     from paper_2609_27373_amd.pipeline import WisePipeline
     seen = set()
     for d in (64, 96, 128):
@@ -172,8 +173,8 @@ def test_group_density_covers_every_group_shape(lib):
                     continue
                 rows = wise.wise_sparse_group_rows(S(head_dim=d, block=block, seq_len=n))
                 if rows > 0:
-                    seen.add((block, rows))
-                    assert (block, rows) in WisePipeline.GROUP_DENSITY, (d, block, n, rows)
+                    seen.add((block, rows, d))
+                    assert (block, rows, d) in WisePipeline.GROUP_DENSITY, (d, block, n, rows)
     assert seen == set(WisePipeline.GROUP_DENSITY)
 
 
